@@ -1,0 +1,239 @@
+"""CPU oracle for the Scalify scaled matmul path (arXiv 2407.17353) - Python side.
+
+TEST INFRASTRUCTURE ONLY: imported by tests/, by __graft_entry__.smoke() and by
+the cpu_baseline leg of bench.py, never by the product package. It wraps the
+plain C oracle in ``scalify_oracle.c`` (table decode, exact nearest-search cast,
+fp64 ascending-k accumulation) with numpy-facing helpers.
+
+Every function states the passage of the paper it follows:
+  * ScaledArray X = X_d * X_s, power-of-two scale held in fp32 (Section 2).
+  * matmul scale rule: divide by a power of two rounded down from sqrt(K)
+    (Section 3.2, Algorithm 3; independent-Gaussian assumption).
+  * dynamic rescale: statistic (amax) -> power of two (rounded down) ->
+    rebalance_scale (Section 3.3, Algorithm 4).
+  * set_scaling / get_data_and_scale (Section 3.1); casts act on data only
+    (Appendix A).
+
+Parity pins for every function live in tests/test_oracle_pins.py.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+E4M3, E5M2, F16, F32 = 0, 1, 2, 3
+RESCALE_NONE, RESCALE_AMAX = 0, 1
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "scalify_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+_lib = None
+
+
+def build() -> str:
+    """Compile the C oracle with gcc (plain IEEE arithmetic: no fast-math, no
+    FMA contraction). Returns the path of the shared library."""
+    cmd = ["gcc", "-O2", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
+           "-shared", "-fPIC", "-Wall", "-o", _LIB + ".tmp", _SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(_LIB + ".tmp", _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB):
+        build()
+    lib = ctypes.CDLL(_LIB)
+    c_i64, c_i32, c_int, c_f32, c_f64 = (ctypes.c_int64, ctypes.c_int32, ctypes.c_int,
+                                         ctypes.c_float, ctypes.c_double)
+    vp = ctypes.c_void_p
+    lib.or_decode.argtypes = [c_int, ctypes.c_uint32]
+    lib.or_decode.restype = c_f64
+    lib.or_cast.argtypes = [c_int, c_int, c_f32]
+    lib.or_cast.restype = ctypes.c_uint32
+    lib.or_cast_array.argtypes = [c_int, c_int, vp, c_i64, vp]
+    lib.or_matmul_scale_log2.argtypes = [c_i64]
+    lib.or_matmul_scale_log2.restype = c_i32
+    lib.or_floor_log2.argtypes = [c_f64]
+    lib.or_floor_log2.restype = c_i32
+    lib.or_matmul_acc.argtypes = [vp, c_int, c_int, c_i64, vp, c_int, c_int, c_i64,
+                                  c_i64, c_i64, c_i64, vp]
+    lib.or_matmul_acc_at.argtypes = [vp, c_int, c_int, c_i64, vp, c_int, c_int, c_i64,
+                                     c_i64, vp, vp, c_i64, vp, vp]
+    lib.or_matmul_epilogue.argtypes = [vp, c_i64, c_f32, c_f32, c_i64, c_int, c_i32, c_int,
+                                       c_int, vp, ctypes.POINTER(c_i32), ctypes.POINTER(c_f32)]
+    lib.or_matmul_epilogue.restype = c_int
+    lib.or_rescale.argtypes = [c_int, vp, c_i64, c_f32, c_int, c_i32, c_int, c_int, vp,
+                               ctypes.POINTER(c_i32), ctypes.POINTER(c_f32)]
+    lib.or_rescale.restype = c_int
+    lib.or_set_scaling.argtypes = [c_int, vp, c_i64, c_f32, c_i32, c_int, c_int, vp]
+    lib.or_set_scaling.restype = c_int
+    lib.or_cast_data.argtypes = [c_int, vp, c_i64, c_int, c_int, vp]
+    lib.or_init()
+    _lib = lib
+    return lib
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _code_dtype(fmt: int):
+    return {E4M3: np.uint8, E5M2: np.uint8, F16: np.uint16, F32: np.float32}[fmt]
+
+
+# --------------------------------------------------------------------------- formats
+
+_tables = {}
+
+
+def decode(fmt: int, codes) -> np.ndarray:
+    """Closed-form decode of FP8 (OCP E4M3 / E5M2) or FP16 codes to float64
+    (Section 1 / Appendix A formats)."""
+    lib = _load()
+    codes = np.asarray(codes)
+    if fmt not in _tables:
+        tab_size = 65536 if fmt == F16 else 256
+        _tables[fmt] = np.array([lib.or_decode(fmt, c) for c in range(tab_size)], dtype=np.float64)
+    return _tables[fmt][codes.astype(np.int64)]
+
+
+def cast(fmt: int, x, saturate: bool = True) -> np.ndarray:
+    """Round fp32 values to FP8/FP16 codes: exact nearest search over the
+    representable values, ties to the even code, OCP saturation rules
+    (stage 2 of the two-stage quantization, Section 2)."""
+    lib = _load()
+    x = np.ascontiguousarray(np.asarray(x, dtype=np.float32))
+    out = np.empty(x.shape, dtype=_code_dtype(fmt))
+    lib.or_cast_array(fmt, int(bool(saturate)), _ptr(x), x.size, _ptr(out))
+    return out
+
+
+def matmul_scale_log2(K: int) -> int:
+    """e_c = log2 of sqrt(K) rounded down to a power of two (Section 3.2)."""
+    return int(_load().or_matmul_scale_log2(int(K)))
+
+
+def floor_log2(x: float) -> int:
+    return int(_load().or_floor_log2(float(x)))
+
+
+# --------------------------------------------------------------------------- matmul
+
+def _operand(codes: np.ndarray, trans: bool):
+    codes = np.ascontiguousarray(codes, dtype=np.uint8)
+    return codes, codes.shape[1]
+
+
+def matmul_acc(A: np.ndarray, fa: int, ta: bool, B: np.ndarray, fb: int, tb: bool) -> np.ndarray:
+    """fp32 accumulator of the FP8 dot_general: fp64 sum over ascending k of the
+    exact products, rounded once to fp32.
+
+    A is stored [M,K] (ta False) or [K,M] (ta True); B is stored [K,N]
+    (tb False) or [N,K] (tb True)."""
+    lib = _load()
+    A, lda = _operand(A, ta)
+    B, ldb = _operand(B, tb)
+    M, K = (A.shape[1], A.shape[0]) if ta else A.shape
+    K2, N = (B.shape[1], B.shape[0]) if tb else B.shape
+    assert K == K2, (K, K2)
+    acc = np.empty((M, N), dtype=np.float32)
+    lib.or_matmul_acc(_ptr(A), fa, int(ta), lda, _ptr(B), fb, int(tb), ldb, M, N, K, _ptr(acc))
+    return acc
+
+
+def matmul_acc_at(A, fa, ta, B, fb, tb, ii, jj):
+    """Accumulator at sampled output positions (ii[p], jj[p]) and the fp64
+    l2 norm of the product terms at each position."""
+    lib = _load()
+    A, lda = _operand(A, ta)
+    B, ldb = _operand(B, tb)
+    K = A.shape[0] if ta else A.shape[1]
+    ii = np.ascontiguousarray(ii, dtype=np.int64)
+    jj = np.ascontiguousarray(jj, dtype=np.int64)
+    acc = np.empty(ii.shape, dtype=np.float32)
+    tn = np.empty(ii.shape, dtype=np.float64)
+    lib.or_matmul_acc_at(_ptr(A), fa, int(ta), lda, _ptr(B), fb, int(tb), ldb, K,
+                         _ptr(ii), _ptr(jj), ii.size, _ptr(acc), _ptr(tn))
+    return acc, tn
+
+
+def matmul_epilogue(acc: np.ndarray, s_a: float, s_b: float, K: int, mode: int = RESCALE_AMAX,
+                    target_log2: int = 0, saturate: bool = True, out_fmt: int = E4M3):
+    """Scale propagation (Section 3.2) + dynamic amax rescale (Section 3.3) +
+    cast (Section 2, stage 2) applied to an fp32 accumulator.
+
+    Returns (codes, e_out, amax): output scale is 2**e_out; amax is
+    max |acc * 2^-e_c| over non-NaN elements."""
+    lib = _load()
+    acc = np.ascontiguousarray(acc, dtype=np.float32)
+    out = np.empty(acc.shape, dtype=_code_dtype(out_fmt))
+    e_out = ctypes.c_int32(0)
+    amax = ctypes.c_float(0)
+    rc = lib.or_matmul_epilogue(_ptr(acc), acc.size, s_a, s_b, int(K), mode, target_log2,
+                                int(bool(saturate)), out_fmt, _ptr(out),
+                                ctypes.byref(e_out), ctypes.byref(amax))
+    if rc != 0:
+        raise ValueError("input scales must be finite powers of two")
+    return out, int(e_out.value), float(amax.value)
+
+
+def matmul(A, fa, ta, s_a, B, fb, tb, s_b, mode=RESCALE_AMAX, target_log2=0, saturate=True,
+           out_fmt=E4M3):
+    """Full scaled matmul on ScaledArray operands: accumulate, then epilogue.
+    Returns (codes, e_out, amax, acc)."""
+    acc = matmul_acc(A, fa, ta, B, fb, tb)
+    K = A.shape[0] if ta else A.shape[1]
+    codes, e_out, amax = matmul_epilogue(acc, s_a, s_b, K, mode, target_log2, saturate, out_fmt)
+    return codes, e_out, amax, acc
+
+
+# --------------------------------------------------------------------------- rescale / cast
+
+def rescale(data: np.ndarray, in_fmt: int, s_in: float, mode: int = RESCALE_AMAX,
+            target_log2: int = 0, saturate: bool = True, out_fmt: int = E4M3):
+    """Dynamic rescale of a ScaledArray (Section 3.3): amax of the decoded data
+    -> power of two rounded down -> rebalance_scale -> cast. Returns
+    (codes, e_out, amax)."""
+    lib = _load()
+    data = np.ascontiguousarray(data, dtype=_code_dtype(in_fmt))
+    out = np.empty(data.shape, dtype=_code_dtype(out_fmt))
+    e_out = ctypes.c_int32(0)
+    amax = ctypes.c_float(0)
+    rc = lib.or_rescale(in_fmt, _ptr(data), data.size, s_in, mode, target_log2,
+                        int(bool(saturate)), out_fmt, _ptr(out), ctypes.byref(e_out),
+                        ctypes.byref(amax))
+    if rc != 0:
+        raise ValueError("input scale must be a finite power of two")
+    return out, int(e_out.value), float(amax.value)
+
+
+def set_scaling(data: np.ndarray, in_fmt: int, s_in: float, e_new: int, saturate: bool = True,
+                out_fmt: int = E4M3) -> np.ndarray:
+    """set_scaling (Section 3.1): output scale 2^e_new, data rescaled by the
+    ratio of old and new scales, then cast."""
+    lib = _load()
+    data = np.ascontiguousarray(data, dtype=_code_dtype(in_fmt))
+    out = np.empty(data.shape, dtype=_code_dtype(out_fmt))
+    rc = lib.or_set_scaling(in_fmt, _ptr(data), data.size, s_in, e_new, int(bool(saturate)),
+                            out_fmt, _ptr(out))
+    if rc != 0:
+        raise ValueError("bad scale")
+    return out
+
+
+def cast_data(data: np.ndarray, in_fmt: int, out_fmt: int, saturate: bool = True) -> np.ndarray:
+    """Cast operator on the data component only; the scale is unchanged
+    (Appendix A)."""
+    lib = _load()
+    data = np.ascontiguousarray(data, dtype=_code_dtype(in_fmt))
+    out = np.empty(data.shape, dtype=_code_dtype(out_fmt))
+    lib.or_cast_data(in_fmt, _ptr(data), data.size, int(bool(saturate)), out_fmt, _ptr(out))
+    return out

@@ -1,0 +1,483 @@
+/*
+ * CPU oracle for the Scalify scaled matmul path (arXiv 2407.17353).
+ *
+ * TEST INFRASTRUCTURE ONLY. Only tests/, __graft_entry__.smoke() and the
+ * cpu_baseline leg of bench.py may load this library. The product path
+ * (the HIP library) never calls it and shares no code with it.
+ *
+ * Plain, slow, obviously correct. Every number format is decoded by a table
+ * built from its closed-form definition; every cast is an exact nearest
+ * search over the sorted list of representable values; every matmul sums
+ * products in fp64 in ascending k and rounds once to fp32.
+ *
+ * What each function follows in the paper:
+ *   - ScaledArray X = X_d * X_s with a power-of-two scale simulated in fp32
+ *     (Section 2, "Scaled array representation and quantization").
+ *   - Two-stage quantization: unit-scale the data, round the scale to a power
+ *     of two and correct q(X_d) (Section 2).
+ *   - Matmul scale propagation under the independent-Gaussian assumption,
+ *     with power-of-two rounding down of the scale (Section 3.2 and
+ *     Algorithm 3).
+ *   - Dynamic rescaling: statistic -> power of two -> rebalance_scale
+ *     (Section 3.3, Algorithm 4), statistic = amax.
+ *   - set_scaling / get_data_and_scale (Section 3.1).
+ *   - FP8 E4M3 / E5M2 and FP16 formats (Section 1, Appendix A), OCP variants.
+ *
+ * Readings of the paper where it is silent are listed in the design notes
+ * of the repository; the ones used here are restated next to the code.
+ */
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <math.h>
+
+enum { OR_E4M3 = 0, OR_E5M2 = 1, OR_F16 = 2, OR_F32 = 3 };
+enum { OR_RESCALE_NONE = 0, OR_RESCALE_AMAX = 1 };
+
+/* ------------------------------------------------------------------------ */
+/* Number formats: closed-form decode (OCP FP8 E4M3 / E5M2, IEEE binary16).  */
+/* ------------------------------------------------------------------------ */
+
+/* E4M3 (OCP "fn"): s|eeee|mmm, bias 7, no infinities, NaN = s.1111.111. */
+double or_decode_e4m3(uint32_t c)
+{
+    int s = (c >> 7) & 1, e = (c >> 3) & 15, m = c & 7;
+    double v;
+    if (e == 15 && m == 7) return NAN;
+    if (e == 0) v = m * ldexp(1.0, -9);               /* subnormal: m/8 * 2^-6 */
+    else v = (1.0 + m / 8.0) * ldexp(1.0, e - 7);
+    return s ? -v : v;
+}
+
+/* E5M2: s|eeeee|mm, bias 15, IEEE-like: e=31 is Inf (m=0) or NaN. */
+double or_decode_e5m2(uint32_t c)
+{
+    int s = (c >> 7) & 1, e = (c >> 2) & 31, m = c & 3;
+    double v;
+    if (e == 31) return m ? NAN : (s ? -INFINITY : INFINITY);
+    if (e == 0) v = m * ldexp(1.0, -16);              /* subnormal: m/4 * 2^-14 */
+    else v = (1.0 + m / 4.0) * ldexp(1.0, e - 15);
+    return s ? -v : v;
+}
+
+/* IEEE binary16: s|eeeee|mmmmmmmmmm, bias 15. */
+double or_decode_f16(uint32_t h)
+{
+    int s = (h >> 15) & 1, e = (h >> 10) & 31, m = h & 1023;
+    double v;
+    if (e == 31) return m ? NAN : (s ? -INFINITY : INFINITY);
+    if (e == 0) v = m * ldexp(1.0, -24);
+    else v = (1.0 + m / 1024.0) * ldexp(1.0, e - 15);
+    return s ? -v : v;
+}
+
+double or_decode(int fmt, uint32_t code)
+{
+    switch (fmt) {
+    case OR_E4M3: return or_decode_e4m3(code & 0xFF);
+    case OR_E5M2: return or_decode_e5m2(code & 0xFF);
+    case OR_F16:  return or_decode_f16(code & 0xFFFF);
+    default: { float f; uint32_t u = code; memcpy(&f, &u, 4); return (double)f; }
+    }
+}
+
+void or_decode_table8(int fmt, double* out256)
+{
+    for (uint32_t c = 0; c < 256; ++c) out256[c] = or_decode(fmt, c);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Cast: exact nearest search, ties to the even code.                        */
+/* ------------------------------------------------------------------------ */
+
+/* Sorted non-negative finite values of a format with their codes. The list is
+ * extended by one "virtual" value: the next value above the largest finite
+ * one, as if the exponent range were unbounded. Rounding to it means the
+ * input overflowed. Its code is max_code + 1, so the even-code tie rule
+ * applies to it like to any other candidate. */
+typedef struct {
+    int n;              /* number of entries incl. the virtual one */
+    double* val;        /* ascending */
+    uint32_t* code;
+    uint32_t max_code;  /* largest finite positive code */
+    uint32_t nan_code;  /* canonical positive NaN */
+    uint32_t inf_code;  /* positive infinity, 0 if the format has none */
+    int sign_shift;     /* 7 for FP8, 15 for FP16 */
+} or_grid;
+
+static or_grid g_grid[3];
+static int g_grid_ready = 0;
+
+static void grid_build(or_grid* g, int fmt)
+{
+    uint32_t ncodes = (fmt == OR_F16) ? 0x8000u : 0x80u;   /* positive half */
+    g->val = (double*)malloc(sizeof(double) * (ncodes + 1));
+    g->code = (uint32_t*)malloc(sizeof(uint32_t) * (ncodes + 1));
+    g->n = 0;
+    g->max_code = 0;
+    /* Positive codes decode to non-decreasing values in code order for all
+     * three formats; collect the finite ones. */
+    for (uint32_t c = 0; c < ncodes; ++c) {
+        double v = or_decode(fmt, c);
+        if (!isfinite(v)) continue;
+        g->val[g->n] = v;
+        g->code[g->n] = c;
+        g->n++;
+        g->max_code = c;
+    }
+    /* Virtual overflow value: max + one unit in the last place at max. */
+    {
+        double vmax = g->val[g->n - 1];
+        double prev = g->val[g->n - 2];
+        /* ulp at max equals the spacing of the top binade; the value below
+         * max is in the same binade for all three formats. */
+        g->val[g->n] = vmax + (vmax - prev);
+        g->code[g->n] = g->max_code + 1;
+        g->n++;
+    }
+    if (fmt == OR_E4M3) { g->nan_code = 0x7F; g->inf_code = 0; g->sign_shift = 7; }
+    else if (fmt == OR_E5M2) { g->nan_code = 0x7F; g->inf_code = 0x7C; g->sign_shift = 7; }
+    else { g->nan_code = 0x7E00; g->inf_code = 0x7C00; g->sign_shift = 15; }
+}
+
+static void grids_init(void)
+{
+    if (g_grid_ready) return;
+    /* Built once, before any parallel region uses it. */
+    grid_build(&g_grid[OR_E4M3], OR_E4M3);
+    grid_build(&g_grid[OR_E5M2], OR_E5M2);
+    grid_build(&g_grid[OR_F16], OR_F16);
+    g_grid_ready = 1;
+}
+
+void or_init(void) { grids_init(); }
+
+/* Round the exact value of x (an fp32) to format fmt.
+ * NaN -> canonical NaN with the sign of x. +-Inf and overflow: saturate to
+ * +-max when sat != 0; otherwise E4M3 gives NaN, E5M2 and FP16 give +-Inf.
+ * Subnormals of the target are kept; -0 stays -0. */
+uint32_t or_cast(int fmt, int sat, float x)
+{
+    const or_grid* g;
+    uint32_t sign;
+    double a;
+    int lo, hi;
+    grids_init();
+    g = &g_grid[fmt];
+    sign = signbit(x) ? (1u << g->sign_shift) : 0u;
+    if (isnan(x)) return g->nan_code | sign;
+    if (isinf(x)) {
+        if (sat) return g->max_code | sign;
+        return (g->inf_code ? g->inf_code : g->nan_code) | sign;
+    }
+    a = fabs((double)x);
+    /* Largest index lo with val[lo] <= a (val[0] = 0). */
+    lo = 0; hi = g->n - 1;
+    if (a >= g->val[hi]) {
+        lo = hi;
+    } else {
+        while (hi - lo > 1) {
+            int mid = (lo + hi) / 2;
+            if (g->val[mid] <= a) lo = mid; else hi = mid;
+        }
+    }
+    {
+        int pick;
+        if (g->val[lo] == a || lo == g->n - 1) {
+            pick = lo;
+        } else {
+            /* Bracketed by val[lo] < a < val[lo+1]; the midpoint of two
+             * grid values is exact in fp64, so this comparison is exact. */
+            double mid = 0.5 * (g->val[lo] + g->val[lo + 1]);
+            if (a < mid) pick = lo;
+            else if (a > mid) pick = lo + 1;
+            else pick = (g->code[lo] & 1u) ? lo + 1 : lo;   /* tie: even code */
+        }
+        if (pick == g->n - 1) {   /* rounded to the virtual value: overflow */
+            if (sat) return g->max_code | sign;
+            return (g->inf_code ? g->inf_code : g->nan_code) | sign;
+        }
+        return g->code[pick] | sign;
+    }
+}
+
+void or_cast_array(int fmt, int sat, const float* x, int64_t n, void* out)
+{
+    int64_t i;
+    grids_init();
+    if (fmt == OR_F16) {
+        uint16_t* o = (uint16_t*)out;
+        #pragma omp parallel for schedule(static)
+        for (i = 0; i < n; ++i) o[i] = (uint16_t)or_cast(fmt, sat, x[i]);
+    } else {
+        uint8_t* o = (uint8_t*)out;
+        #pragma omp parallel for schedule(static)
+        for (i = 0; i < n; ++i) o[i] = (uint8_t)or_cast(fmt, sat, x[i]);
+    }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Power-of-two helpers (Section 2: the scale is always 2^k, E8M0).          */
+/* ------------------------------------------------------------------------ */
+
+/* floor(log2 |x|) for finite nonzero x, from frexp: x = f * 2^e, f in [0.5,1). */
+int32_t or_floor_log2(double x)
+{
+    int e;
+    frexp(fabs(x), &e);
+    return e - 1;
+}
+
+/* Exponent of a power-of-two scale. Returns 0 and sets *ok = 0 if s is not a
+ * finite positive power of two (a precondition violation). */
+int32_t or_scale_exponent(float s, int* ok)
+{
+    int e;
+    double f;
+    if (!(s > 0.0f) || !isfinite(s)) { *ok = 0; return 0; }
+    f = frexp((double)s, &e);
+    *ok = (f == 0.5);
+    return e - 1;
+}
+
+/* Matmul scale rule (Section 3.2, Algorithm 3): under the independent
+ * unit-Gaussian assumption Var(sum_k a_k b_k) = K, so the output is divided
+ * by sqrt(K); that constant is rounded DOWN to a power of two, as the paper
+ * does for every scale. Result: the largest e with 2^e <= sqrt(K), i.e. with
+ * 4^e <= K. Integer search, no floating-point sqrt. */
+int32_t or_matmul_scale_log2(int64_t K)
+{
+    int32_t e = 0;
+    if (K < 1) return 0;
+    while (e < 31 && ((int64_t)1 << (2 * (e + 1))) <= K) e++;
+    return e;
+}
+
+/* E8M0 range of a scale exponent (Section 2: 8-bit power-of-two scale). */
+static int32_t clamp_e8m0(int32_t e)
+{
+    if (e < -127) return -127;
+    if (e > 127) return 127;
+    return e;
+}
+
+/* ------------------------------------------------------------------------ */
+/* FP8 dot_general with fp64 accumulation.                                   */
+/* ------------------------------------------------------------------------ */
+
+/* Element (i,k) of A and (k,j) of B under the storage convention:
+ * trans = 0: stored [rows][ld]; trans = 1: stored transposed [cols][ld]. */
+#define A_AT(i, k) (ta ? A[(int64_t)(k) * lda + (i)] : A[(int64_t)(i) * lda + (k)])
+#define B_AT(k, j) (tb ? B[(int64_t)(j) * ldb + (k)] : B[(int64_t)(k) * ldb + (j)])
+
+/* acc[i*N+j] = fp32( sum_{k=0}^{K-1} dec(A[i,k]) * dec(B[k,j]) ), summed in
+ * fp64 in ascending k. Rows are independent; OpenMP splits rows only. */
+void or_matmul_acc(const uint8_t* A, int fa, int ta, int64_t lda,
+                   const uint8_t* B, int fb, int tb, int64_t ldb,
+                   int64_t M, int64_t N, int64_t K, float* acc)
+{
+    double da[256], db[256];
+    int64_t i;
+    or_decode_table8(fa, da);
+    or_decode_table8(fb, db);
+    #pragma omp parallel for schedule(dynamic, 1)
+    for (i = 0; i < M; ++i) {
+        int64_t j, k;
+        for (j = 0; j < N; ++j) {
+            double s = 0.0;
+            for (k = 0; k < K; ++k) s += da[A_AT(i, k)] * db[B_AT(k, j)];
+            acc[i * N + j] = (float)s;
+        }
+    }
+}
+
+/* The same sum for a list of (i, j) pairs, plus the fp64 l2 norm of the
+ * product terms sqrt(sum_k (a_ik b_kj)^2), which sets the accumulator
+ * tolerance. */
+void or_matmul_acc_at(const uint8_t* A, int fa, int ta, int64_t lda,
+                      const uint8_t* B, int fb, int tb, int64_t ldb,
+                      int64_t K, const int64_t* ii, const int64_t* jj, int64_t n,
+                      float* acc, double* term_norm)
+{
+    double da[256], db[256];
+    int64_t p;
+    or_decode_table8(fa, da);
+    or_decode_table8(fb, db);
+    #pragma omp parallel for schedule(static)
+    for (p = 0; p < n; ++p) {
+        int64_t i = ii[p], j = jj[p], k;
+        double s = 0.0, q = 0.0;
+        for (k = 0; k < K; ++k) {
+            double t = da[A_AT(i, k)] * db[B_AT(k, j)];
+            s += t;
+            if (isfinite(t)) q += t * t;
+        }
+        acc[p] = (float)s;
+        if (term_norm) term_norm[p] = sqrt(q);
+    }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Dynamic rescale (Section 3.3) and the matmul epilogue.                    */
+/* ------------------------------------------------------------------------ */
+
+/* amax = max |x| over non-NaN elements; *any = 0 if every element is NaN. */
+float or_amax(const float* x, int64_t n, int* any)
+{
+    float m = 0.0f;
+    int64_t i;
+    *any = 0;
+    for (i = 0; i < n; ++i) {
+        float a = fabsf(x[i]);
+        if (isnan(a)) continue;
+        *any = 1;
+        if (a > m) m = a;
+    }
+    return m;
+}
+
+/* Rescale exponent e_r from the statistic: the power of two is rounded down
+ * (floor(log2 amax)), then shifted by the target t, so that the rescaled
+ * amax lies in [2^t, 2^(t+1)). No rescale (0) when there is nothing to
+ * measure: amax 0, +Inf, or no non-NaN element. */
+int32_t or_rescale_exponent(float amax, int any, int32_t t)
+{
+    if (!any || amax == 0.0f || isinf(amax)) return 0;
+    return or_floor_log2((double)amax) - t;
+}
+
+/* Shared tail of the matmul epilogue and of rescale: given fp32 values v
+ * whose true value is v * 2^e_in, choose the output scale exponent and cast.
+ *   mode NONE: e_want = e_in;  mode AMAX: e_want = e_in + e_r.
+ *   e_out = clamp(e_want) to the E8M0 range;  data' = ldexp(v, e_in - e_out).
+ * One power-of-two shift of the exact fp32 value, then one rounding. */
+static int32_t finish(const float* v, int64_t n, int32_t e_in, int mode, int32_t t,
+                      int sat, int out_fmt, void* out, float* amax_out)
+{
+    int any;
+    float amax = or_amax(v, n, &any);
+    int32_t e_r = (mode == OR_RESCALE_AMAX) ? or_rescale_exponent(amax, any, t) : 0;
+    int32_t e_out = clamp_e8m0(e_in + e_r);
+    int32_t shift = e_in - e_out;
+    int64_t i;
+    grids_init();
+    if (amax_out) *amax_out = amax;
+    #pragma omp parallel for schedule(static)
+    for (i = 0; i < n; ++i) {
+        float d = ldexpf(v[i], shift);
+        uint32_t c = or_cast(out_fmt, sat, d);
+        if (out_fmt == OR_F16) ((uint16_t*)out)[i] = (uint16_t)c;
+        else ((uint8_t*)out)[i] = (uint8_t)c;
+    }
+    return e_out;
+}
+
+/* Epilogue of the scaled matmul (Section 3.2 propagation + Section 3.3
+ * dynamic rescale + stage-2 cast of Section 2), applied to an fp32
+ * accumulator acc[n] (n = M*N).
+ *   e_c  = matmul scale rule for K; data = acc * 2^-e_c is exact.
+ *   value of data = data * 2^(e_a + e_b + e_c).
+ * Returns 0 on success, -1 on a non-power-of-two input scale.
+ * Outputs: codes, *e_out (output scale = 2^e_out), *amax (of acc*2^-e_c). */
+int or_matmul_epilogue(const float* acc, int64_t n, float s_a, float s_b, int64_t K,
+                       int mode, int32_t t, int sat, int out_fmt,
+                       void* out, int32_t* e_out, float* amax)
+{
+    int ok_a = 1, ok_b = 1;
+    int32_t e_a = or_scale_exponent(s_a, &ok_a);
+    int32_t e_b = or_scale_exponent(s_b, &ok_b);
+    int32_t e_c = or_matmul_scale_log2(K);
+    float* data;
+    int64_t i;
+    if (!ok_a || !ok_b) return -1;
+    data = (float*)malloc(sizeof(float) * (size_t)(n > 0 ? n : 1));
+    for (i = 0; i < n; ++i) data[i] = ldexpf(acc[i], -e_c);
+    /* The propagated data carries 2^(e_a+e_b+e_c). finish() shifts acc-based
+     * data by e_in - e_out, which equals -(e_r) plus any clamp correction. */
+    *e_out = finish(data, n, e_a + e_b + e_c, mode, t, sat, out_fmt, out, amax);
+    free(data);
+    return 0;
+}
+
+/* Full scaled matmul: accumulate then epilogue. acc_out may be NULL. */
+int or_matmul(const uint8_t* A, int fa, int ta, int64_t lda, float s_a,
+              const uint8_t* B, int fb, int tb, int64_t ldb, float s_b,
+              int64_t M, int64_t N, int64_t K,
+              int mode, int32_t t, int sat, int out_fmt,
+              void* out, int32_t* e_out, float* amax, float* acc_out)
+{
+    float* acc = acc_out ? acc_out : (float*)malloc(sizeof(float) * (size_t)(M * N > 0 ? M * N : 1));
+    int rc;
+    or_matmul_acc(A, fa, ta, lda, B, fb, tb, ldb, M, N, K, acc);
+    rc = or_matmul_epilogue(acc, M * N, s_a, s_b, K, mode, t, sat, out_fmt, out, e_out, amax);
+    if (!acc_out) free(acc);
+    return rc;
+}
+
+/* Decode an array of codes (or fp32 bits) of format fmt to fp32. FP8 and
+ * FP16 values are exact in fp32. */
+static void decode_to_f32(int fmt, const void* in, int64_t n, float* out)
+{
+    int64_t i;
+    for (i = 0; i < n; ++i) {
+        uint32_t c;
+        if (fmt == OR_F32) { memcpy(&out[i], (const float*)in + i, 4); continue; }
+        c = (fmt == OR_F16) ? ((const uint16_t*)in)[i] : ((const uint8_t*)in)[i];
+        out[i] = (float)or_decode(fmt, c);
+    }
+}
+
+/* Dynamic rescale of a ScaledArray (Section 3.3 with rebalance_scale, plus
+ * the cast when the output format differs): value = dec(in) * s_in.
+ * AMAX: e_r from the amax of dec(in); s_out = s_in * 2^e_r (clamped);
+ * data' = dec(in) * 2^-(e_out - e_in). NONE: scale kept, data cast. */
+int or_rescale(int in_fmt, const void* in, int64_t n, float s_in,
+               int mode, int32_t t, int sat, int out_fmt,
+               void* out, int32_t* e_out, float* amax)
+{
+    int ok = 1;
+    int32_t e_in = or_scale_exponent(s_in, &ok);
+    float* v;
+    if (!ok) return -1;
+    v = (float*)malloc(sizeof(float) * (size_t)(n > 0 ? n : 1));
+    decode_to_f32(in_fmt, in, n, v);
+    *e_out = finish(v, n, e_in, mode, t, sat, out_fmt, out, amax);
+    free(v);
+    return 0;
+}
+
+/* set_scaling (Section 3.1): the output gets scale 2^e_new; the data is
+ * rescaled by the ratio of the old and new scales, then cast. */
+int or_set_scaling(int in_fmt, const void* in, int64_t n, float s_in,
+                   int32_t e_new, int sat, int out_fmt, void* out)
+{
+    int ok = 1;
+    int32_t e_in = or_scale_exponent(s_in, &ok);
+    float* v;
+    int64_t i;
+    if (!ok || e_new < -127 || e_new > 127) return -1;
+    v = (float*)malloc(sizeof(float) * (size_t)(n > 0 ? n : 1));
+    decode_to_f32(in_fmt, in, n, v);
+    for (i = 0; i < n; ++i) {
+        uint32_t c = or_cast(out_fmt, sat, ldexpf(v[i], e_in - e_new));
+        if (out_fmt == OR_F16) ((uint16_t*)out)[i] = (uint16_t)c;
+        else ((uint8_t*)out)[i] = (uint8_t)c;
+    }
+    free(v);
+    return 0;
+}
+
+/* Cast operator on the data only (Appendix A: casts act on data, the scale
+ * is unchanged). */
+void or_cast_data(int in_fmt, const void* in, int64_t n, int sat, int out_fmt, void* out)
+{
+    float* v = (float*)malloc(sizeof(float) * (size_t)(n > 0 ? n : 1));
+    int64_t i;
+    decode_to_f32(in_fmt, in, n, v);
+    for (i = 0; i < n; ++i) {
+        uint32_t c = or_cast(out_fmt, sat, v[i]);
+        if (out_fmt == OR_F16) ((uint16_t*)out)[i] = (uint16_t)c;
+        else ((uint8_t*)out)[i] = (uint8_t)c;
+    }
+    free(v);
+}
