@@ -1,0 +1,178 @@
+#!/usr/bin/env python3
+"""Benchmark of the scaled-FP8 matmul with fused dynamic rescale and cast.
+
+One step = one scalify_matmul call on the headline workload: M = N = K = 8192,
+E4M3 x E4M3 -> E4M3 with the amax rescale (prologue + fused GEMM/amax +
+epilogue cast), inputs already resident in HBM. Prints ONE JSON line with
+the whole-call throughput (TFLOP/s), the roofline of the dominant kernel
+(the fused GEMM, timed live with HIP events recorded by the library on its
+stream) and the CPU oracle timed on a bounded sample of the same workload.
+
+  python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
+  python bench.py --sweep      # also time every benchmark configuration
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "scaled-FP8 GEMM TFLOP/s incl. rescale+cast; % of MI355X FP8 MFMA peak"
+PEAK_FP8_TFLOPS = 5000.0      # MI355X dense FP8 MFMA, 256 CU x 2.4 GHz x 8192 FLOP/clk
+PEAK_HBM_GBS = 8000.0
+FMT_NAME = {0: "e4m3", 1: "e5m2", 2: "f16"}
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=12.0,
+                   help="target CPU time of the oracle sample")
+    p.add_argument("--sweep", action="store_true", help="also time every configuration")
+    return p.parse_args()
+
+
+def time_case(case, steps, warmup, dev, ws=None):
+    """Time `steps` scalify_matmul calls of one GemmCase. Returns a dict with
+    ms per call (event-timed over the whole timed region) and the mean
+    duration of the fused GEMM kernel and of the epilogue cast."""
+    import torch
+    from paper_2407_17353_amd import binding as sc
+
+    A = case.make_a(dev)
+    B = case.make_b(dev)
+    a = sc.ScaledArray(A, case.fa, sc.scale_tensor(case.a_scale_log2, dev), case.ta)
+    b = sc.ScaledArray(B, case.fb, sc.scale_tensor(case.b_scale_log2, dev), case.tb)
+    out = sc.empty_scaled(case.M, case.N, case.fout, dev)
+    need = sc.scalify_matmul_workspace_size(case.M, case.N, case.fout, case.mode)
+    if ws is None or ws.numel() < need:
+        ws = sc.workspace(need, dev)
+    stream = torch.cuda.current_stream()
+    for _ in range(warmup):
+        sc.scalify_matmul(a, b, out, rescale=case.mode, ws=ws)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t0.record(stream)
+    for k in range(steps):
+        sc.scalify_matmul(a, b, out, rescale=case.mode, ws=ws, events=evs[k])
+    t1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = t0.elapsed_time(t1)
+    gemm_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / steps
+    cast_ms = sum(e[1].elapsed_time(e[2]) for e in evs) / steps
+    del A, B, a, b, out
+    return {"ms_per_step": total_ms / steps, "wall_ms_per_step": wall * 1e3 / steps,
+            "gemm_ms": gemm_ms, "cast_ms": cast_ms}, ws
+
+
+def cpu_baseline(case, target_s):
+    """The oracle as it stands (fp64 accumulate + epilogue), timed on the
+    first m rows of the same workload, m chosen for about target_s seconds."""
+    import numpy as np
+    from oracle import oracle as orc
+
+    A = case.make_a("cuda:0").cpu().numpy()   # the very bytes the GPU run used
+    B = case.make_b("cuda:0").cpu().numpy()
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+
+    def run(m):
+        t = time.perf_counter()
+        orc.matmul(A[:m], case.fa, False, 2.0 ** case.a_scale_log2, B, case.fb, False,
+                   2.0 ** case.b_scale_log2, out_fmt=case.fout)
+        return time.perf_counter() - t
+
+    m = max(1, threads)
+    t = run(m)
+    if t < target_s / 4:
+        m = int(min(case.M, max(m, m * target_s / max(t, 1e-3))) // threads * threads) or threads
+        t = run(m)
+    flops = 2.0 * m * case.N * case.K
+    return {"value": flops / t / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": f"rows 0..{m - 1} of A (a {m}x{case.N}x{case.K} scaled matmul: fp64 "
+                      f"accumulation, amax rescale and cast), {t:.1f} s",
+            "seconds": round(t, 2), "rows": m}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(the sharding design is described in DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2407_17353_amd import binding as sc
+    from paper_2407_17353_amd import workloads as wl
+
+    if not os.path.exists(sc.LIB_PATH):
+        from paper_2407_17353_amd import build as hip_build
+        hip_build.build()
+    sc.load_library()
+    dev = "cuda:0"
+    case = wl.config_4(8192, wl.E4M3)[0]
+    res, ws = time_case(case, args.steps, args.warmup, dev)
+    flops = case.flops
+    value = flops / (res["ms_per_step"] * 1e-3) / 1e12
+    gemm_tflops = flops / (res["gemm_ms"] * 1e-3) / 1e12
+    line = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(res["ms_per_step"], 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp8e4m3",
+        "data": "synthetic",
+        "config": {"workload": "scaled matmul 8192x8192x8192, E4M3 x E4M3 -> E4M3, amax "
+                               "rescale + saturating RNE cast (square sweep, 8192 case)",
+                   "M": case.M, "N": case.N, "K": case.K, "a_fmt": "e4m3", "b_fmt": "e4m3",
+                   "out_fmt": "e4m3", "layout": "A [M][K], B [K][N]",
+                   "scales_log2": [case.a_scale_log2, case.b_scale_log2]},
+        "pct_of_peak": round(100.0 * value / PEAK_FP8_TFLOPS, 2),
+        "gemm_kernel_us": round(res["gemm_ms"] * 1e3, 2),
+        "epilogue_cast_us": round(res["cast_ms"] * 1e3, 2),
+        "roofline": {"bound": "mfma", "achieved": round(gemm_tflops, 2),
+                     "peak": PEAK_FP8_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(gemm_tflops / PEAK_FP8_TFLOPS, 4), "traffic": None},
+    }
+    if args.sweep:
+        sweep = []
+        for cfg, cases in wl.all_configs().items():
+            for c in cases:
+                r, ws = time_case(c, max(5, args.steps // 5), 2, dev, ws)
+                tf = c.flops / (r["ms_per_step"] * 1e-3) / 1e12
+                row = {"config": cfg, "name": c.name, "M": c.M, "N": c.N, "K": c.K,
+                       "us": round(r["ms_per_step"] * 1e3, 1), "tflops": round(tf, 1),
+                       "pct_peak": round(100 * tf / PEAK_FP8_TFLOPS, 1),
+                       "gemm_us": round(r["gemm_ms"] * 1e3, 1),
+                       "cast_us": round(r["cast_ms"] * 1e3, 1)}
+                sweep.append(row)
+                print(json.dumps(row), file=sys.stderr, flush=True)
+        os.makedirs(os.path.join(ROOT, "gpurun_out"), exist_ok=True)
+        with open(os.path.join(ROOT, "gpurun_out", "sweep.json"), "w") as f:
+            json.dump(sweep, f, indent=1)
+    del ws
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(case, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,172 @@
+/*
+ * scalify.h - C ABI of the MI355X (gfx950) scaled-FP8 matmul library.
+ *
+ * Implements the hot path of Scalify's scale propagation (Balanca et al.,
+ * "Scalify: scale propagation for efficient low-precision LLM training",
+ * arXiv 2407.17353):
+ *   - a ScaledArray is a pair (data X_d, scale X_s) with X = X_d * X_s, where
+ *     X_s is a power of two held in one fp32 (Section 2; Section 3.1,
+ *     Algorithm 2);
+ *   - the scaled matmul propagates the output scale s_a * s_b * c with
+ *     c = sqrt(K) rounded DOWN to a power of two, dividing the data by c
+ *     (Section 3.2, Algorithm 3: static rule from scales and shapes under the
+ *     independent-Gaussian assumption; scales rounded down);
+ *   - dynamic rescaling: statistic of the data -> power of two (rounded down)
+ *     -> rebalance_scale (Section 3.3, Algorithm 4); the statistic is amax;
+ *   - set_scaling and get_data_and_scale (Section 3.1);
+ *   - casts act on the data component only (Appendix A, cast operators);
+ *   - FP8 formats E4M3 / E5M2 (Section 1, Appendix A; OCP encodings on gfx950)
+ *     and FP16 (E5M10) outputs.
+ *
+ * Conventions for every entry point
+ *   - All data and scale pointers are DEVICE pointers owned by the caller.
+ *     The library allocates nothing and keeps no state between calls;
+ *     concurrent calls are safe when they use distinct workspaces.
+ *   - Work is enqueued on `stream` (a hipStream_t passed as void*, NULL = the
+ *     default stream). No call synchronises the host or reads a scale back.
+ *   - Argument errors are detected on the host before any launch; they return
+ *     a status and leave every output untouched. A failed launch returns
+ *     SCALIFY_ERR_HIP.
+ *   - Numeric specials are not errors: NaN inputs give NaN outputs, amax
+ *     ignores NaN, Inf amax or zero amax keep the propagated scale.
+ *   - Preconditions not checked by the kernels: input scales are finite
+ *     powers of two within the E8M0 range [2^-127, 2^127]. A NULL input scale
+ *     means scale 1 (get_data_and_scale of an unscaled array, Section 3.1).
+ */
+#ifndef SCALIFY_H
+#define SCALIFY_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    SCALIFY_OK = 0,
+    SCALIFY_ERR_NULL = 1,      /* a required pointer is NULL */
+    SCALIFY_ERR_DTYPE = 2,     /* unsupported data type or combination */
+    SCALIFY_ERR_SHAPE = 3,     /* inconsistent or negative sizes */
+    SCALIFY_ERR_LAYOUT = 4,    /* unsupported storage layout or aliasing */
+    SCALIFY_ERR_ALIGN = 5,     /* data pointer or leading dimension not 16-byte aligned */
+    SCALIFY_ERR_WORKSPACE = 6, /* workspace missing or too small */
+    SCALIFY_ERR_VALUE = 7,     /* scalar argument out of range */
+    SCALIFY_ERR_HIP = 8        /* a HIP launch failed */
+} scalify_status;
+
+typedef enum {
+    SCALIFY_E4M3 = 0, /* OCP FP8 E4M3: bias 7, max 448, no Inf, NaN = S.1111.111 */
+    SCALIFY_E5M2 = 1, /* OCP FP8 E5M2: bias 15, max 57344, Inf and NaN */
+    SCALIFY_F16 = 2,  /* IEEE binary16 (E5M10) */
+    SCALIFY_F32 = 3   /* IEEE binary32 (inputs of rescale / cast / set_scaling only) */
+} scalify_dtype;
+
+typedef enum {
+    SCALIFY_RESCALE_NONE = 0, /* static propagation rule only */
+    SCALIFY_RESCALE_AMAX = 1  /* dynamic power-of-two rescale from the amax */
+} scalify_rescale_mode;
+
+/* A ScaledArray (Section 2, Section 3.1): value = decode(data) * (*scale).
+ * Logical shape rows x cols.
+ *   trans = 0: element (r, c) is stored at data[r * ld + c]  (ld >= cols)
+ *   trans = 1: element (r, c) is stored at data[c * ld + r]  (ld >= rows)
+ * The storage must hold every stored row in full: (stored rows) * ld
+ * elements. `scale` points to ONE fp32 power of two on the device; NULL is
+ * allowed for inputs (scale 1) and is an error for outputs. */
+typedef struct {
+    void* data;
+    float* scale;
+    int32_t dtype; /* scalify_dtype */
+    int32_t trans;
+    int64_t rows;
+    int64_t cols;
+    int64_t ld; /* in elements */
+} scalify_scaled_array;
+
+typedef struct {
+    int32_t out_dtype;   /* SCALIFY_E4M3 | SCALIFY_E5M2 | SCALIFY_F16 */
+    int32_t rescale;     /* scalify_rescale_mode */
+    int32_t target_log2; /* t: AMAX puts the rescaled amax in [2^t, 2^(t+1)); default 0 */
+    int32_t saturate;    /* 1: overflow and +-Inf -> +-max; 0: E4M3 -> NaN, E5M2/F16 -> +-Inf */
+    float* acc_out;      /* optional device [M][N] fp32: the raw accumulator sum_k a_ik b_kj */
+    float* amax_out;     /* optional device fp32: amax of acc * 2^-e_c over non-NaN elements */
+    void** events;       /* optional host array of 3 hipEvent_t recorded on the stream: before
+                            the GEMM kernel, after it, and after the epilogue cast (timing of
+                            the fused GEMM without host synchronisation); NULL = none */
+} scalify_matmul_opts;
+
+/* Exponent e_c of the matmul scale rule (Section 3.2, Algorithm 3): the
+ * largest e with 2^e <= sqrt(K) (sqrt(K) rounded down to a power of two),
+ * computed with integers. Returns 0 for K < 1. Host only. */
+int32_t scalify_matmul_scale_log2(int64_t K);
+
+/* Bytes of device workspace scalify_matmul needs for an M x N output with
+ * the given output type and rescale mode: a 256-byte header plus the
+ * pre-cast intermediate (M rows of N rounded up to 16 elements; 2 bytes per
+ * element for FP8 outputs, 4 for FP16). Returns 0 for invalid arguments. */
+size_t scalify_matmul_workspace_size(int64_t M, int64_t N, int32_t out_dtype, int32_t rescale);
+
+/* Scaled matmul on ScaledArray operands (Section 3.2, Algorithm 3; FP8
+ * matmul with mixed input formats and higher-precision accumulation,
+ * Appendix A), with the dynamic rescale (Section 3.3) fused:
+ *   acc   = sum_k dec(a)[i,k] * dec(b)[k,j]        fp32 accumulation (MFMA)
+ *   e_c   = scalify_matmul_scale_log2(K)
+ *   AMAX: e_r = floor(log2 amax(acc * 2^-e_c)) - target_log2
+ *         (0 when that amax is 0 or +Inf or every element is NaN)
+ *   NONE: e_r = 0
+ *   e_out = clamp(e_a + e_b + e_c + e_r, -127, 127)        (E8M0 range)
+ *   out.data  = RNE(acc * 2^(e_a + e_b - e_out)) in out.dtype (saturating
+ *               when opts.saturate), *out.scale = 2^e_out
+ * so that dec(out) * s_out = s_a * s_b * acc up to the final rounding.
+ *
+ * a: M x K, b: K x N, out: M x N. a and b are E4M3 or E5M2 in any mix and
+ * either storage order (trans 0/1). out.trans must be 0 and out.dtype must
+ * equal opts->out_dtype. All data pointers 16-byte aligned, every ld a
+ * multiple of 16 elements (8 for an FP16 out). workspace: device memory of
+ * at least scalify_matmul_workspace_size(M, N, ...) bytes, 256-byte aligned,
+ * not shared with a concurrent call. Determinism: reruns are bit-identical.
+ * M, N or K may be 0 (K = 0 gives an all-zero output). */
+scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scaled_array* b,
+                              scalify_scaled_array* out, const scalify_matmul_opts* opts,
+                              void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of device workspace scalify_rescale needs (a 256-byte header). */
+size_t scalify_rescale_workspace_size(int64_t n);
+
+/* Dynamic rescale of a ScaledArray (Section 3.3, Algorithm 4: statistic,
+ * power of two rounded down, rebalance_scale), with a cast when out.dtype
+ * differs from in.dtype:
+ *   AMAX: e_r = floor(log2 amax(dec(in))) - target_log2 (0 for amax 0 / +Inf /
+ *         all NaN); NONE: e_r = 0
+ *   e_out = clamp(e_in + e_r, -127, 127); out.data = RNE(dec(in) * 2^(e_in - e_out))
+ * in.dtype: any scalify_dtype; out.dtype: E4M3, E5M2 or F16. in and out have
+ * the same shape and trans and are stored contiguously (ld = cols, or rows
+ * when trans = 1). out may alias in only when both have the same element
+ * size; out.scale may alias in.scale. workspace >= 256 bytes. */
+scalify_status scalify_rescale(const scalify_scaled_array* in, scalify_scaled_array* out,
+                               int32_t mode, int32_t target_log2, int32_t saturate,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
+/* Cast of the data component only; the scale is copied (Appendix A cast
+ * operators): out.data = RNE(dec(in)), *out.scale = *in.scale (1 if NULL).
+ * Same layout rules as scalify_rescale. */
+scalify_status scalify_cast(const scalify_scaled_array* in, scalify_scaled_array* out,
+                            int32_t saturate, void* stream);
+
+/* set_scaling (Section 3.1): the output gets scale 2^new_scale_log2 and the
+ * data is rescaled by the ratio of the old and new scales:
+ *   out.data = RNE(dec(in) * 2^(e_in - new_scale_log2)), *out.scale = 2^new_scale_log2.
+ * new_scale_log2 in [-127, 127]. out.scale must not alias in.scale. Same
+ * layout rules as scalify_rescale. */
+scalify_status scalify_set_scaling(const scalify_scaled_array* in, scalify_scaled_array* out,
+                                   int32_t new_scale_log2, int32_t saturate, void* stream);
+
+/* Human-readable name of a status code (static string). */
+const char* scalify_status_string(int32_t status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SCALIFY_H */

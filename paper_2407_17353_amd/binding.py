@@ -1,0 +1,220 @@
+"""Python binding of libscalify.so (include/scalify.h): argument marshalling only.
+
+Every step of the scaled matmul, rescale and cast runs in the HIP kernels of
+the library; this module turns torch device tensors into the C structs, picks
+the current HIP stream, allocates workspaces with torch and raises on a
+non-OK status. There is no fallback: if the library is missing, importing it
+raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import torch
+
+E4M3, E5M2, F16, F32 = 0, 1, 2, 3
+RESCALE_NONE, RESCALE_AMAX = 0, 1
+
+STATUS_NAMES = {0: "SCALIFY_OK", 1: "SCALIFY_ERR_NULL", 2: "SCALIFY_ERR_DTYPE",
+                3: "SCALIFY_ERR_SHAPE", 4: "SCALIFY_ERR_LAYOUT", 5: "SCALIFY_ERR_ALIGN",
+                6: "SCALIFY_ERR_WORKSPACE", 7: "SCALIFY_ERR_VALUE", 8: "SCALIFY_ERR_HIP"}
+
+# storage element type of each format (codes are carried as raw bits)
+STORAGE_DTYPE = {E4M3: torch.uint8, E5M2: torch.uint8, F16: torch.int16, F32: torch.float32}
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libscalify.so")
+
+
+class ScalifyError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {STATUS_NAMES.get(status, status)} "
+                         f"({string_of(status)})")
+
+
+class CScaledArray(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("scale", ctypes.c_void_p), ("dtype", ctypes.c_int32),
+                ("trans", ctypes.c_int32), ("rows", ctypes.c_int64), ("cols", ctypes.c_int64),
+                ("ld", ctypes.c_int64)]
+
+
+class CMatmulOpts(ctypes.Structure):
+    _fields_ = [("out_dtype", ctypes.c_int32), ("rescale", ctypes.c_int32),
+                ("target_log2", ctypes.c_int32), ("saturate", ctypes.c_int32),
+                ("acc_out", ctypes.c_void_p), ("amax_out", ctypes.c_void_p),
+                ("events", ctypes.c_void_p)]
+
+
+EXPORTED = ("scalify_matmul_scale_log2", "scalify_matmul_workspace_size", "scalify_matmul",
+            "scalify_rescale_workspace_size", "scalify_rescale", "scalify_cast",
+            "scalify_set_scaling", "scalify_status_string")
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libscalify.so (built by paper_2407_17353_amd/build.py). Raises
+    FileNotFoundError when it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise FileNotFoundError(f"{path} is missing: run paper_2407_17353_amd/build.py")
+    lib = ctypes.CDLL(path)
+    P = ctypes.POINTER
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    lib.scalify_matmul_scale_log2.argtypes = [i64]
+    lib.scalify_matmul_scale_log2.restype = i32
+    lib.scalify_matmul_workspace_size.argtypes = [i64, i64, i32, i32]
+    lib.scalify_matmul_workspace_size.restype = ctypes.c_size_t
+    lib.scalify_matmul.argtypes = [P(CScaledArray), P(CScaledArray), P(CScaledArray),
+                                   P(CMatmulOpts), vp, ctypes.c_size_t, vp]
+    lib.scalify_matmul.restype = ctypes.c_int
+    lib.scalify_rescale_workspace_size.argtypes = [i64]
+    lib.scalify_rescale_workspace_size.restype = ctypes.c_size_t
+    lib.scalify_rescale.argtypes = [P(CScaledArray), P(CScaledArray), i32, i32, i32, vp,
+                                    ctypes.c_size_t, vp]
+    lib.scalify_rescale.restype = ctypes.c_int
+    lib.scalify_cast.argtypes = [P(CScaledArray), P(CScaledArray), i32, vp]
+    lib.scalify_cast.restype = ctypes.c_int
+    lib.scalify_set_scaling.argtypes = [P(CScaledArray), P(CScaledArray), i32, i32, vp]
+    lib.scalify_set_scaling.restype = ctypes.c_int
+    lib.scalify_status_string.argtypes = [i32]
+    lib.scalify_status_string.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def string_of(status: int) -> str:
+    return load_library().scalify_status_string(int(status)).decode()
+
+
+@dataclass
+class ScaledArray:
+    """A ScaledArray (data, scale) with value = decode(data) * scale
+    (Section 2 of the paper). `data` is the STORED matrix as a 2-D tensor
+    whose rows are contiguous (stride(1) == 1; stride(0) is the leading
+    dimension); with trans=True it stores the transpose of the logical
+    matrix. `scale` is a one-element float32 device tensor or None (scale 1)."""
+    data: torch.Tensor
+    fmt: int
+    scale: Optional[torch.Tensor] = None
+    trans: bool = False
+
+    @property
+    def shape(self):
+        r, c = self.data.shape
+        return (c, r) if self.trans else (r, c)
+
+    def c_struct(self) -> CScaledArray:
+        d = self.data
+        if d.dim() != 2:
+            raise ValueError("ScaledArray data must be 2-D")
+        if d.shape[0] * d.shape[1] > 0 and d.stride(1) != 1:
+            raise ValueError("ScaledArray rows must be contiguous")
+        rows, cols = self.shape
+        ld = d.stride(0) if d.numel() else 0
+        return CScaledArray(d.data_ptr() if d.numel() else None,
+                            self.scale.data_ptr() if self.scale is not None else None,
+                            int(self.fmt), int(bool(self.trans)), rows, cols, ld)
+
+
+def _stream_handle(stream) -> Optional[int]:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+def _check(status: int, where: str):
+    if status != 0:
+        raise ScalifyError(status, where)
+
+
+def scalify_matmul_scale_log2(K: int) -> int:
+    return int(load_library().scalify_matmul_scale_log2(int(K)))
+
+
+def scalify_matmul_workspace_size(M: int, N: int, out_fmt: int, rescale: int = RESCALE_AMAX) -> int:
+    return int(load_library().scalify_matmul_workspace_size(M, N, out_fmt, rescale))
+
+
+def scalify_rescale_workspace_size(n: int) -> int:
+    return int(load_library().scalify_rescale_workspace_size(n))
+
+
+def workspace(nbytes: int, device) -> torch.Tensor:
+    """Device workspace of nbytes, 256-byte aligned (torch allocations are)."""
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+def scalify_matmul(a: ScaledArray, b: ScaledArray, out: ScaledArray, *, rescale: int = RESCALE_AMAX,
+                   target_log2: int = 0, saturate: bool = True, acc_out: torch.Tensor = None,
+                   amax_out: torch.Tensor = None, ws: torch.Tensor = None, stream=None,
+                   events=None) -> None:
+    """Scaled matmul (Section 3.2) with the fused dynamic rescale and cast
+    (Section 3.3); see scalify_matmul in include/scalify.h. `events`: an
+    optional sequence of 3 torch.cuda.Event(enable_timing=True) recorded
+    before the GEMM kernel, after it and after the epilogue cast."""
+    lib = load_library()
+    M, _ = a.shape
+    _, N = b.shape
+    if ws is None:
+        ws = workspace(scalify_matmul_workspace_size(M, N, out.fmt, rescale), a.data.device)
+    ev_arr = None
+    if events is not None:
+        ev_arr = (ctypes.c_void_p * 3)(*[e.cuda_event for e in events])
+    opts = CMatmulOpts(int(out.fmt), int(rescale), int(target_log2), int(bool(saturate)),
+                       acc_out.data_ptr() if acc_out is not None else None,
+                       amax_out.data_ptr() if amax_out is not None else None,
+                       ctypes.cast(ev_arr, ctypes.c_void_p) if ev_arr is not None else None)
+    ca, cb, co = a.c_struct(), b.c_struct(), out.c_struct()
+    st = lib.scalify_matmul(ctypes.byref(ca), ctypes.byref(cb), ctypes.byref(co), ctypes.byref(opts),
+                            ws.data_ptr(), ws.numel(), _stream_handle(stream))
+    _check(st, "scalify_matmul")
+
+
+def scalify_rescale(x: ScaledArray, out: ScaledArray, *, mode: int = RESCALE_AMAX, target_log2: int = 0,
+                    saturate: bool = True, ws: torch.Tensor = None, stream=None) -> None:
+    """Dynamic rescale (Section 3.3): amax -> power of two -> rebalance, plus cast."""
+    lib = load_library()
+    if ws is None:
+        ws = workspace(scalify_rescale_workspace_size(x.data.numel()), x.data.device)
+    ci, co = x.c_struct(), out.c_struct()
+    st = lib.scalify_rescale(ctypes.byref(ci), ctypes.byref(co), int(mode), int(target_log2),
+                             int(bool(saturate)), ws.data_ptr(), ws.numel(), _stream_handle(stream))
+    _check(st, "scalify_rescale")
+
+
+def scalify_cast(x: ScaledArray, out: ScaledArray, *, saturate: bool = True, stream=None) -> None:
+    """Cast of the data component; the scale is copied (Appendix A)."""
+    ci, co = x.c_struct(), out.c_struct()
+    st = load_library().scalify_cast(ctypes.byref(ci), ctypes.byref(co), int(bool(saturate)),
+                                     _stream_handle(stream))
+    _check(st, "scalify_cast")
+
+
+def scalify_set_scaling(x: ScaledArray, out: ScaledArray, new_scale_log2: int, *, saturate: bool = True,
+                        stream=None) -> None:
+    """set_scaling (Section 3.1): output scale 2^new_scale_log2, data rebalanced."""
+    ci, co = x.c_struct(), out.c_struct()
+    st = load_library().scalify_set_scaling(ctypes.byref(ci), ctypes.byref(co), int(new_scale_log2),
+                                            int(bool(saturate)), _stream_handle(stream))
+    _check(st, "scalify_set_scaling")
+
+
+# ----------------------------------------------------------------------------- helpers
+
+def empty_scaled(rows: int, cols: int, fmt: int, device, ld: int = None) -> ScaledArray:
+    """Output ScaledArray [rows, cols] with leading dimension ld (default: cols
+    rounded up to 16 elements) and a fresh scale tensor."""
+    if ld is None:
+        ld = max(16, (cols + 15) // 16 * 16)
+    storage = torch.empty((rows, ld), dtype=STORAGE_DTYPE[fmt], device=device)
+    return ScaledArray(storage[:, :cols], fmt, torch.empty(1, dtype=torch.float32, device=device))
+
+
+def scale_tensor(log2: int, device) -> torch.Tensor:
+    return torch.tensor([2.0 ** log2], dtype=torch.float32, device=device)

@@ -1,0 +1,247 @@
+// HBM-bound kernels of the scaled-matmul epilogue and of the standalone
+// ScaledArray operations:
+//   * prologue: clears the amax word and snapshots input scale exponents;
+//   * epilogue_cast: the grid-wide dependent half of the fused dynamic
+//     rescale (Section 3.3): reads the global amax, derives the power-of-two
+//     rescale exponent (rounded down), writes the output scale, and casts the
+//     GEMM's pre-cast intermediate with round-to-nearest-even;
+//   * amax: |x| max of an existing ScaledArray's data, as an integer max over
+//     magnitude keys (no decode in the hot loop);
+//   * elementwise: rebalance / set_scaling / cast of a ScaledArray's data.
+// Every kernel moves 16 elements per thread per iteration with 128-bit
+// loads and stores and walks the array with a grid-stride loop.
+#include "codec.h"
+#include "kernels.h"
+
+namespace scalify {
+
+typedef unsigned int u4 __attribute__((ext_vector_type(4)));
+
+constexpr int EW_THREADS = 256;
+
+__global__ void prologue_kernel(uint32_t* hdr, const float* s0, const float* s1) {
+  if (threadIdx.x == 0) {
+    hdr[0] = 0u;
+    hdr[1] = (uint32_t)(pow2_exponent(s0) + pow2_exponent(s1));
+  }
+}
+
+hipError_t launch_prologue(uint32_t* hdr, const float* s0, const float* s1, hipStream_t s) {
+  hipLaunchKernelGGL(prologue_kernel, dim3(1), dim3(64), 0, s, hdr, s0, s1);
+  return hipGetLastError();
+}
+
+// Load 16 consecutive elements of format F as raw codes / fp32 bits.
+template <int F>
+__device__ __forceinline__ void load16(const void* base, int64_t e, uint32_t (&c)[16]) {
+  if (F == kE4M3 || F == kE5M2) {
+    const u4 v = *(const u4*)((const uint8_t*)base + e);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) c[i] = (v[i >> 2] >> (8 * (i & 3))) & 0xFFu;
+  } else if (F == kF16) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const u4 v = *(const u4*)((const uint16_t*)base + e + 8 * h);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) c[8 * h + i] = (v[i >> 1] >> (16 * (i & 1))) & 0xFFFFu;
+    }
+  } else {
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      const u4 v = *(const u4*)((const uint32_t*)base + e + 4 * h);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) c[4 * h + i] = v[i];
+    }
+  }
+}
+
+template <int F>
+__device__ __forceinline__ uint32_t load1(const void* base, int64_t e) {
+  if (F == kE4M3 || F == kE5M2) return ((const uint8_t*)base)[e];
+  if (F == kF16) return ((const uint16_t*)base)[e];
+  return ((const uint32_t*)base)[e];
+}
+
+template <int F>
+__device__ __forceinline__ uint32_t to_bits(uint32_t c) {
+  if constexpr (F == kF32) return c;
+  else return decode_bits<F>(c);
+}
+
+// Store 16 codes of output format F (FP8: 16 B, FP16: 32 B).
+template <int F>
+__device__ __forceinline__ void store16(void* base, int64_t e, const uint32_t (&c)[16]) {
+  if (F == kF16) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      u4 v;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = c[8 * h + 2 * i] | (c[8 * h + 2 * i + 1] << 16);
+      *(u4*)((uint16_t*)base + e + 8 * h) = v;
+    }
+  } else {
+    u4 v;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      v[i] = c[4 * i] | (c[4 * i + 1] << 8) | (c[4 * i + 2] << 16) | (c[4 * i + 3] << 24);
+    *(u4*)((uint8_t*)base + e) = v;
+  }
+}
+
+template <int F>
+__device__ __forceinline__ void store1(void* base, int64_t e, uint32_t c) {
+  if (F == kF16) ((uint16_t*)base)[e] = (uint16_t)c;
+  else ((uint8_t*)base)[e] = (uint8_t)c;
+}
+
+// ---------------------------------------------------------------- GEMM epilogue cast
+
+template <int INTER32, int OUTF>
+__global__ __launch_bounds__(EW_THREADS) void epilogue_cast_kernel(EpilogueParams p) {
+  const uint32_t amax_raw = p.hdr[0];  // max |acc| bits
+  const int e_ab = (int)p.hdr[1];
+  int e_r = 0;
+  if (p.mode == 1 && amax_raw != 0u && amax_raw < 0x7F800000u)
+    e_r = floor_log2_bits(amax_raw) - p.e_c - p.target;
+  const int e_out = clamp_e8m0(e_ab + p.e_c + e_r);
+  const int shift = e_out - e_ab;  // data' = acc * 2^-shift
+  const bool sat = p.sat != 0;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    *p.out_scale = pow2_float(e_out);
+    if (p.amax_out) *p.amax_out = __uint_as_float(amax_raw) * pow2_float(-p.e_c);
+  }
+  const int64_t cpr = (p.N + 15) / 16;
+  const int64_t total = (int64_t)p.M * cpr;
+  for (int64_t idx = (int64_t)blockIdx.x * EW_THREADS + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * EW_THREADS) {
+    const int64_t m = idx / cpr;
+    const int n = (int)(idx - m * cpr) * 16;
+    uint32_t c[16];
+    if (INTER32) {
+      load16<kF32>(p.inter, m * p.ldw + n, c);
+    } else {
+      load16<kF16>(p.inter, m * p.ldw + n, c);  // 16-bit containers
+#pragma unroll
+      for (int i = 0; i < 16; ++i) c[i] <<= 16;
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) c[i] = cast_bits<OUTF>(c[i], shift, sat);
+    if (n + 16 <= p.N) {
+      store16<OUTF>(p.out, m * p.ldc + n, c);
+    } else {
+      for (int i = 0; i < 16; ++i)
+        if (n + i < p.N) store1<OUTF>(p.out, m * p.ldc + n + i, c[i]);
+    }
+  }
+}
+
+static int grid_for(int64_t work) {
+  int64_t b = (work + EW_THREADS - 1) / EW_THREADS;
+  if (b < 1) b = 1;
+  if (b > 8192) b = 8192;
+  return (int)b;
+}
+
+hipError_t launch_epilogue_cast(const EpilogueParams& p, int inter32, int out_dtype,
+                                hipStream_t s) {
+  const int grid = grid_for((int64_t)p.M * ((p.N + 15) / 16));
+  const dim3 g(grid), b(EW_THREADS);
+  if (inter32) {
+    hipLaunchKernelGGL((epilogue_cast_kernel<1, kF16>), g, b, 0, s, p);
+  } else if (out_dtype == kE4M3) {
+    hipLaunchKernelGGL((epilogue_cast_kernel<0, kE4M3>), g, b, 0, s, p);
+  } else {
+    hipLaunchKernelGGL((epilogue_cast_kernel<0, kE5M2>), g, b, 0, s, p);
+  }
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- amax
+
+template <int F>
+__global__ __launch_bounds__(EW_THREADS) void amax_kernel(const void* in, int64_t n,
+                                                           uint32_t* hdr) {
+  __shared__ uint32_t red[EW_THREADS / 64];
+  uint32_t kmax = 0;
+  const int64_t nv = n / 16;
+  for (int64_t v = (int64_t)blockIdx.x * EW_THREADS + threadIdx.x; v < nv;
+       v += (int64_t)gridDim.x * EW_THREADS) {
+    uint32_t c[16];
+    load16<F>(in, v * 16, c);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) kmax = max(kmax, magnitude_key<F>(c[i]));
+  }
+  if (blockIdx.x == 0)
+    for (int64_t e = nv * 16 + threadIdx.x; e < n; e += EW_THREADS)
+      kmax = max(kmax, magnitude_key<F>(load1<F>(in, e)));
+  for (int off = 32; off > 0; off >>= 1) kmax = max(kmax, (uint32_t)__shfl_xor((int)kmax, off, 64));
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = kmax;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t k = red[0];
+    for (int w = 1; w < EW_THREADS / 64; ++w) k = max(k, red[w]);
+    atomicMax(hdr, to_bits<F>(k));
+  }
+}
+
+hipError_t launch_amax(const void* in, int in_dtype, int64_t n, uint32_t* hdr, hipStream_t s) {
+  const dim3 g(grid_for(n / 16)), b(EW_THREADS);
+  switch (in_dtype) {
+    case kE4M3: hipLaunchKernelGGL((amax_kernel<kE4M3>), g, b, 0, s, in, n, hdr); break;
+    case kE5M2: hipLaunchKernelGGL((amax_kernel<kE5M2>), g, b, 0, s, in, n, hdr); break;
+    case kF16: hipLaunchKernelGGL((amax_kernel<kF16>), g, b, 0, s, in, n, hdr); break;
+    default: hipLaunchKernelGGL((amax_kernel<kF32>), g, b, 0, s, in, n, hdr); break;
+  }
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- rescale / cast / set_scaling
+
+template <int INF, int OUTF>
+__global__ __launch_bounds__(EW_THREADS) void elementwise_kernel(ElemParams p) {
+  int shift = 0, e_out = 0;
+  if (p.rule != RULE_COPY) {
+    const int e_in = p.hdr ? (int)p.hdr[1] : pow2_exponent(p.in_scale);
+    if (p.rule == RULE_AMAX) e_out = clamp_e8m0(e_in + rescale_exponent(p.hdr[0], p.target));
+    else if (p.rule == RULE_KEEP) e_out = e_in;
+    else e_out = p.e_fixed;
+    shift = e_out - e_in;
+  }
+  const bool sat = p.sat != 0;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    if (p.rule == RULE_COPY) *p.out_scale = p.in_scale ? *p.in_scale : 1.0f;
+    else *p.out_scale = pow2_float(e_out);
+  }
+  const int64_t nv = p.n / 16;
+  for (int64_t v = (int64_t)blockIdx.x * EW_THREADS + threadIdx.x; v < nv;
+       v += (int64_t)gridDim.x * EW_THREADS) {
+    uint32_t c[16];
+    load16<INF>(p.in, v * 16, c);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) c[i] = cast_bits<OUTF>(to_bits<INF>(c[i]), shift, sat);
+    store16<OUTF>(p.out, v * 16, c);
+  }
+  if (blockIdx.x == 0)
+    for (int64_t e = nv * 16 + threadIdx.x; e < p.n; e += EW_THREADS)
+      store1<OUTF>(p.out, e, cast_bits<OUTF>(to_bits<INF>(load1<INF>(p.in, e)), shift, sat));
+}
+
+template <int INF>
+static void launch_elem_out(const ElemParams& p, int out_dtype, dim3 g, dim3 b, hipStream_t s) {
+  if (out_dtype == kE4M3) hipLaunchKernelGGL((elementwise_kernel<INF, kE4M3>), g, b, 0, s, p);
+  else if (out_dtype == kE5M2) hipLaunchKernelGGL((elementwise_kernel<INF, kE5M2>), g, b, 0, s, p);
+  else hipLaunchKernelGGL((elementwise_kernel<INF, kF16>), g, b, 0, s, p);
+}
+
+hipError_t launch_elementwise(const ElemParams& p, int in_dtype, int out_dtype, hipStream_t s) {
+  const dim3 g(grid_for(p.n / 16)), b(EW_THREADS);
+  switch (in_dtype) {
+    case kE4M3: launch_elem_out<kE4M3>(p, out_dtype, g, b, s); break;
+    case kE5M2: launch_elem_out<kE5M2>(p, out_dtype, g, b, s); break;
+    case kF16: launch_elem_out<kF16>(p, out_dtype, g, b, s); break;
+    default: launch_elem_out<kF32>(p, out_dtype, g, b, s); break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace scalify

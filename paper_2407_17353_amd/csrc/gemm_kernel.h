@@ -1,0 +1,329 @@
+// Scaled FP8 GEMM for gfx950 (MI355X): the FP8 dot_general with fp32
+// accumulation of the scaled matmul (Scalify, Section 3.2 / Algorithm 3;
+// mixed E4M3/E5M2 inputs and higher-precision accumulation, Appendix A),
+// with its epilogue fused: the amax statistic of the dynamic rescale
+// (Section 3.3) and a compact pre-cast intermediate for the cast kernel
+// that follows (the rescale exponent needs the amax of the whole output).
+//
+// Design (per workgroup of 256 threads = 4 wave64):
+//   * 256 x 256 output tile, K consumed in 128-byte steps; each wave owns a
+//     128 x 128 quadrant = 8 x 8 tiles of v_mfma_f32_16x16x128_f8f6f4.
+//   * A and B k-slices (32 KiB each) stream HBM -> LDS with
+//     global_load_lds_dwordx4 (16 B per lane, no VGPR staging), double
+//     buffered: 4 x 32 KiB = 128 KiB of the 160 KiB LDS.
+//   * Operands whose K is contiguous in memory ("KC" tiles, 128 B rows) are
+//     read with ds_read_b128; operands whose M or N is contiguous ("MC"
+//     tiles, 256 B rows along k) are read with ds_read_b64_tr_b8, which
+//     transposes 8x16 byte blocks across 16 lanes, so every storage order
+//     feeds the MFMA without a separate transpose pass.
+//   * Both tile kinds are XOR-swizzled in 16-byte chunks so that fragment
+//     reads hit distinct LDS banks; the swizzle is applied on the global
+//     side of the loads because global_load_lds writes lane i at base+16*i.
+//   * The MFMA is issued with B as its first operand, so each lane ends up
+//     holding 4 consecutive output columns: the epilogue stores 4/8/16-byte
+//     vectors per lane without an LDS round trip.
+//   * Tile order: workgroup ids are remapped so that each XCD (ids are
+//     dealt round-robin over the 8 XCDs) walks a contiguous range of tiles,
+//     grouped 4 tile-rows high, so the tiles that run together on one XCD
+//     share A and B panels in its L2.
+#pragma once
+#include "codec.h"
+#include "kernels.h"
+
+#include <type_traits>
+
+namespace scalify {
+
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v2i __attribute__((ext_vector_type(2)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+#define LDS_AS __attribute__((address_space(3)))
+
+constexpr int BM = 256, BN = 256, BK = 128, NTHR = 256;
+constexpr int TILE_BYTES = 32768;
+
+// 16-byte chunk swizzles (see file comment). KC: 16 consecutive rows read
+// the same logical chunk from 16 distinct bank groups. MC: the 8 rows a
+// 16-lane group reads with one transposing load, and the rows of the
+// neighbouring group, fall on distinct chunks.
+__device__ __forceinline__ int swz_kc(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+__device__ __forceinline__ int swz_mc(int k) { return (k & 7) | (((k >> 5) & 1) << 3); }
+
+// Buffer resource of one operand: base, num_records = bytes of the stored
+// matrix, raw (stride 0) gfx9 descriptor word. Loads at offsets >= the
+// matrix size return zeros instead of touching memory.
+__device__ __forceinline__ v4i make_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t a = (uint64_t)base;
+  v4i r;
+  r.x = (int)(uint32_t)a;
+  r.y = (int)(uint32_t)(a >> 32);
+  r.z = (int)bytes;
+  r.w = 0x00020000;
+  return r;
+}
+
+// One buffer_load_dwordx4 ... lds: lane i's 16 bytes land at M0 + 16 i.
+// M0 has no other user in these kernels (no LDS-DMA builtins, no indexed
+// register moves), so clobbering it here is safe.
+// Issued as inline asm so that the compiler does not order every later LDS
+// read behind it; completion is awaited explicitly (s_waitcnt vmcnt(0))
+// before the barrier that publishes a k-step.
+__device__ __forceinline__ void load_lds16(v4i rsrc, uint32_t voff, uint8_t* lds_base) {
+  const uint32_t lds_addr = (uint32_t)(uintptr_t)(LDS_AS void*)lds_base;
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "buffer_load_dwordx4 %1, %2, 0 offen lds"
+      :
+      : "s"(lds_addr), "v"(voff), "s"(rsrc)
+      : "memory", "m0");
+#pragma clang diagnostic pop
+}
+
+// Per-thread parts of the chunk offsets of one operand tile. Lane i of a
+// wave writes LDS bytes [16 i, 16 i + 16) of its 1 KiB block, so the
+// swizzle is applied to the global address; it depends on the lane and on
+// the parity of the block, so two lane offsets cover all 8 blocks.
+//   KC: tile rows run along M (or N), 128 bytes of K per row; block q of
+//       wave w holds rows 8 (8 w + q) .. +7.
+//   MC: tile rows run along K, 256 bytes of M (or N) per row; block q of
+//       wave w holds k-rows 4 (8 w + q) .. +3.
+struct TileLoader {
+  uint32_t lane_off[2];  // per parity of the block index
+  int kchunk[2];         // KC: k offset (bytes) of the lane's chunk, per parity
+};
+
+template <bool KC>
+__device__ __forceinline__ TileLoader make_loader(uint32_t ld, int wave, int lane) {
+  TileLoader L;
+#pragma unroll
+  for (int par = 0; par < 2; ++par) {
+    if (KC) {
+      const int c = (lane & 7) ^ (lane >> 3) ^ par;
+      L.lane_off[par] = (uint32_t)(lane >> 3) * ld + 16u * (uint32_t)c;
+      L.kchunk[par] = 16 * c;
+    } else {
+      const int c = (lane & 15) ^ (par * 4 + (lane >> 4)) ^ ((wave & 1) << 3);
+      L.lane_off[par] = (uint32_t)(lane >> 4) * ld + 16u * (uint32_t)c;
+      L.kchunk[par] = 0;
+    }
+  }
+  return L;
+}
+
+// Issue the 8 chunk loads (1 KiB per wave instruction) of one operand tile
+// for the k-step starting at k0. Out-of-matrix rows (beyond M or N for KC,
+// beyond K for MC) read zeros through the buffer range check; in the
+// partial last k-step (TAIL) KC chunks that start at or beyond K are sent
+// out of range too, and a chunk straddling K is trimmed by zero_tail.
+template <bool KC, bool TAIL>
+__device__ __forceinline__ void issue_tile(v4i rsrc, const TileLoader& L, uint32_t ld, int row0,
+                                           int k0, int K, uint8_t* lds, int wave) {
+  const uint32_t oob = (uint32_t)rsrc.z;
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    const int blk = wave * 8 + q;
+    uint32_t off;
+    if (KC) {
+      off = (uint32_t)(row0 + blk * 8) * ld + (uint32_t)k0 + L.lane_off[q & 1];
+      if (TAIL && k0 + L.kchunk[q & 1] >= K) off = oob;
+    } else {
+      off = (uint32_t)(k0 + blk * 4) * ld + (uint32_t)row0 + L.lane_off[q & 1];
+    }
+    load_lds16(rsrc, off, lds + blk * 1024);
+  }
+}
+
+// KC tiles when K is not a multiple of 16: zero the bytes k >= krem of the
+// chunk that straddles K (chunks wholly beyond K were loaded as zeros).
+__device__ __forceinline__ void zero_tail_kc(uint8_t* lds, int krem, int tid) {
+  const int r = tid;  // 256 rows, one per thread
+  const int c = krem >> 4;
+  uint8_t* chunk = lds + r * 128 + ((c ^ swz_kc(r)) * 16);
+  for (int b = krem & 15; b < 16; ++b) chunk[b] = 0;
+}
+
+// 32 consecutive k of one row (KC) or one column (MC) of a 16-wide
+// fragment, in the order the MFMA expects: lane l serves row/col (l & 15),
+// k = 32 * (l >> 4) + 0..31.
+template <bool KC>
+__device__ __forceinline__ v8i read_frag(const uint8_t* lds, int base, int lane) {
+  v8i f;
+  if (KC) {
+    const int r = base + (lane & 15);
+    const int g = lane >> 4;
+    const int s = swz_kc(r);
+    const v4i lo = *(const v4i*)(lds + r * 128 + (((2 * g) ^ s) * 16));
+    const v4i hi = *(const v4i*)(lds + r * 128 + (((2 * g + 1) ^ s) * 16));
+    f = v8i{lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+  } else {
+    const int t = lane & 15, g = lane >> 4;
+    const int cn = base >> 4;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const int k = 32 * g + 8 * s + (t >> 1);
+      const int off = k * 256 + ((cn ^ swz_mc(k)) * 16) + (t & 1) * 8;
+      const v2i v = __builtin_amdgcn_ds_read_tr8_b64_v2i32((LDS_AS v2i*)(lds + off));
+      f[2 * s] = v.x;
+      f[2 * s + 1] = v.y;
+    }
+  }
+  return f;
+}
+
+template <int FA, int FB>
+__device__ __forceinline__ v4f mfma(const v8i& bfrag, const v8i& afrag, const v4f& c) {
+  // First operand = B fragment (rows of the MFMA result index N), second =
+  // A fragment: result lane l holds C[m = l & 15][n = 4 * (l >> 4) + i].
+  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(bfrag, afrag, c, FB, FA, 0, 0, 0, 0);
+}
+
+template <int I, int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<I + 1, N>(f);
+  }
+}
+
+template <bool A_MN, bool B_KC, int FA, int FB>
+__device__ __forceinline__ void mma_step(v4f (&acc)[8][8], const uint8_t* cA, const uint8_t* cB,
+                                         int wm, int wn, int lane) {
+  v8i af[8];
+#pragma unroll
+  for (int mi = 0; mi < 8; ++mi) af[mi] = read_frag<!A_MN>(cA, wm + 16 * mi, lane);
+#pragma unroll
+  for (int ni = 0; ni < 8; ++ni) {
+    const v8i bf = read_frag<B_KC>(cB, wn + 16 * ni, lane);
+#pragma unroll
+    for (int mi = 0; mi < 8; ++mi) acc[mi][ni] = mfma<FA, FB>(bf, af[mi], acc[mi][ni]);
+  }
+}
+
+template <bool A_MN, bool B_KC, int FA, int FB, int EPI>
+__global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
+  __shared__ __attribute__((aligned(1024))) uint8_t sA0[TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sB0[TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sA1[TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sB1[TILE_BYTES];
+  __shared__ float red[4];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+  // ---- tile id: XCD-contiguous ranges, then 4-row grouped order
+  const int T = p.tiles_m * p.tiles_n;
+  int t = blockIdx.x;
+  if ((T & 7) == 0) t = (t & 7) * (T >> 3) + (t >> 3);
+  const int G = 4;
+  const int group = t / (G * p.tiles_n);
+  const int first_m = group * G;
+  const int gm = min(p.tiles_m - first_m, G);
+  const int in_group = t - group * G * p.tiles_n;
+  const int m0 = (first_m + in_group % gm) * BM;
+  const int n0 = (in_group / gm) * BN;
+
+  const int M = p.M, N = p.N, K = p.K;
+  const int KT = (K + BK - 1) / BK;
+  const int KT_full = K / BK;         // k-steps entirely inside K
+  const int krem = K - KT_full * BK;  // bytes of the partial last step (0 if none)
+  const uint32_t lda = (uint32_t)p.lda, ldb = (uint32_t)p.ldb;
+
+  // A: KC when stored [M][K], MC when stored [K][M] (row0 = m0 either way).
+  // B: KC when stored [N][K], MC when stored [K][N].
+  const v4i ra = make_rsrc(p.a, p.a_bytes);
+  const v4i rb = make_rsrc(p.b, p.b_bytes);
+  const TileLoader la = make_loader<!A_MN>(lda, wave, lane);
+  const TileLoader lb = make_loader<B_KC>(ldb, wave, lane);
+
+  auto issue = [&](int kt, uint8_t* dA, uint8_t* dB) {
+    if (kt < KT_full) {
+      issue_tile<!A_MN, false>(ra, la, lda, m0, kt * BK, K, dA, wave);
+      issue_tile<B_KC, false>(rb, lb, ldb, n0, kt * BK, K, dB, wave);
+    } else {
+      issue_tile<!A_MN, true>(ra, la, lda, m0, kt * BK, K, dA, wave);
+      issue_tile<B_KC, true>(rb, lb, ldb, n0, kt * BK, K, dB, wave);
+    }
+  };
+  auto fix_tail = [&](int kt, uint8_t* dA, uint8_t* dB) {
+    if (kt == KT_full && (krem & 15)) {
+      if (!A_MN) zero_tail_kc(dA, krem, tid);
+      if (B_KC) zero_tail_kc(dB, krem, tid);
+      __syncthreads();
+    }
+  };
+
+  v4f acc[8][8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+
+  const int wm = (wave >> 1) * 128;  // wave quadrant
+  const int wn = (wave & 1) * 128;
+
+  if (KT > 0) issue(0, sA0, sB0);
+  for (int kt = 0; kt < KT; ++kt) {
+    const bool odd = kt & 1;
+    uint8_t* cA = odd ? sA1 : sA0;
+    uint8_t* cB = odd ? sB1 : sB0;
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    fix_tail(kt, cA, cB);
+    if (kt + 1 < KT) issue(kt + 1, odd ? sA0 : sA1, odd ? sB0 : sB1);
+    mma_step<A_MN, B_KC, FA, FB>(acc, cA, cB, wm, wn, lane);
+  }
+
+  // ---- epilogue: lane holds C[m][n..n+3] for each (mi, ni)
+  float lmax = 0.f;
+  const int mb = m0 + wm + (lane & 15);
+  const int nb = n0 + wn + 4 * (lane >> 4);
+  static_for<0, 64>([&](auto I) {
+    constexpr int mi = decltype(I)::value / 8, ni = decltype(I)::value % 8;
+    const int m = mb + 16 * mi;
+    const int n = nb + 16 * ni;
+    const v4f v = acc[mi][ni];
+    if (m < M && n < N) {
+      lmax = fmaxf(lmax, fabsf(v[0]));
+      if (n + 1 < N) lmax = fmaxf(lmax, fabsf(v[1]));
+      if (n + 2 < N) lmax = fmaxf(lmax, fabsf(v[2]));
+      if (n + 3 < N) lmax = fmaxf(lmax, fabsf(v[3]));
+      if (EPI == EPI_INTER16) {
+        const uint32_t h0 = sticky16(__float_as_uint(v[0])), h1 = sticky16(__float_as_uint(v[1]));
+        const uint32_t h2 = sticky16(__float_as_uint(v[2])), h3 = sticky16(__float_as_uint(v[3]));
+        uint16_t* q = (uint16_t*)p.inter + (int64_t)m * p.ldw + n;
+        *(v2i*)q = v2i{(int)(h0 | (h1 << 16)), (int)(h2 | (h3 << 16))};
+      } else {
+        float* q = (float*)p.inter + (int64_t)m * p.ldw + n;
+        *(v4f*)q = v;
+      }
+      if (p.acc_out) {
+        float* q = p.acc_out + (int64_t)m * N + n;
+        q[0] = v[0];
+        if (n + 1 < N) q[1] = v[1];
+        if (n + 2 < N) q[2] = v[2];
+        if (n + 3 < N) q[3] = v[3];
+      }
+    }
+  });
+  // amax of |acc| over the valid elements (fmaxf ignores NaN): wave
+  // butterfly, then across the 4 waves, then one atomic max per workgroup
+  // on the fp32 bits (non-negative floats order like their bits).
+  for (int off = 32; off > 0; off >>= 1) lmax = fmaxf(lmax, __shfl_xor(lmax, off, 64));
+  if (lane == 0) red[wave] = lmax;
+  __syncthreads();
+  if (tid == 0) {
+    const float wmax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    atomicMax(p.hdr, __float_as_uint(wmax));
+  }
+}
+
+// Launch of one (layout, format, epilogue) family; defined per layout in
+// gemm_<layout>.hip so that the instantiations compile in parallel.
+template <bool A_MN, bool B_KC>
+hipError_t launch_layout(const GemmParams& p, int fa, int fb, int epi, hipStream_t s);
+
+}  // namespace scalify

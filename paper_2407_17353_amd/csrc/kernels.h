@@ -1,0 +1,71 @@
+// Internal interface between the C ABI (scalify_abi.hip) and the kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace scalify {
+
+// Workspace header, in 32-bit words at the start of every workspace:
+//   [0] amax as fp32 bits (atomic max target; zeroed by the prologue)
+//   [1] exponent sum of the input scales (snapshot taken by the prologue, so
+//       that an output scale aliasing an input scale cannot race)
+constexpr size_t kHeaderBytes = 256;
+
+// Pre-cast intermediate written by the GEMM: 16-bit rounding-preserving
+// encoding (FP8 outputs) or the fp32 accumulator (FP16 outputs).
+enum Epi : int { EPI_INTER16 = 0, EPI_INTER32 = 1 };
+
+struct GemmParams {
+  const uint8_t* a;
+  const uint8_t* b;
+  int64_t lda, ldb;
+  uint32_t a_bytes, b_bytes;  // stored-matrix sizes (buffer range limits)
+  int M, N, K;
+  int tiles_m, tiles_n;
+  int e_c;        // matmul scale rule exponent
+  int sat;
+  uint32_t* hdr;  // workspace header
+  void* inter;    // pre-cast intermediate [M][ldw] (EPI_INTER16: u16, EPI_INTER32: f32)
+  int64_t ldw;
+  float* acc_out;  // optional raw accumulator [M][N]
+};
+
+hipError_t launch_gemm(const GemmParams& p, bool a_mn, bool b_kc, int fa, int fb, int epi,
+                       hipStream_t s);
+
+// Prologue: hdr[0] = 0, hdr[1] = exponent(s0) + exponent(s1) (NULL = scale 1).
+hipError_t launch_prologue(uint32_t* hdr, const float* s0, const float* s1, hipStream_t s);
+
+// Cast of the GEMM intermediate [M][ldw] to out [M][ldc]; computes the
+// rescale exponent from hdr and writes *out_scale (and *amax_out).
+struct EpilogueParams {
+  const void* inter;
+  int64_t ldw;
+  void* out;
+  int64_t ldc;
+  int M, N;
+  int e_c, target, sat, mode;
+  const uint32_t* hdr;
+  float* out_scale;
+  float* amax_out;
+};
+hipError_t launch_epilogue_cast(const EpilogueParams& p, int inter32, int out_dtype,
+                                hipStream_t s);
+
+// Elementwise rescale / cast / set_scaling of a contiguous array of n elements.
+enum ScaleRule : int { RULE_AMAX = 0, RULE_KEEP = 1, RULE_FIXED = 2, RULE_COPY = 3 };
+struct ElemParams {
+  const void* in;
+  void* out;
+  int64_t n;
+  int rule;          // RULE_AMAX: from hdr amax; RULE_KEEP: e_out = e_in; RULE_FIXED: e_out = e_fixed;
+                     // RULE_COPY: shift 0 and the raw input scale value is copied
+  int target, sat, e_fixed;
+  const uint32_t* hdr;      // RULE_AMAX / RULE_KEEP (e_in snapshot); may be NULL otherwise
+  const float* in_scale;    // read directly when hdr is NULL
+  float* out_scale;
+};
+hipError_t launch_amax(const void* in, int in_dtype, int64_t n, uint32_t* hdr, hipStream_t s);
+hipError_t launch_elementwise(const ElemParams& p, int in_dtype, int out_dtype, hipStream_t s);
+
+}  // namespace scalify

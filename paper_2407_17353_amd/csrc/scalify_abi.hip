@@ -1,0 +1,243 @@
+// C ABI of the scaled-FP8 matmul library: argument validation on the host,
+// the propagation rule table (exponent arithmetic only), workspace sizing and
+// the launch sequence of each entry point. See include/scalify.h.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/scalify.h"
+#include "kernels.h"
+
+using namespace scalify;
+
+namespace {
+
+bool is_fp8(int32_t d) { return d == SCALIFY_E4M3 || d == SCALIFY_E5M2; }
+bool is_out(int32_t d) { return d == SCALIFY_E4M3 || d == SCALIFY_E5M2 || d == SCALIFY_F16; }
+bool is_any(int32_t d) { return d >= SCALIFY_E4M3 && d <= SCALIFY_F32; }
+int64_t elem_bytes(int32_t d) { return d == SCALIFY_F32 ? 4 : (d == SCALIFY_F16 ? 2 : 1); }
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+constexpr int64_t kMaxDim = (int64_t)1 << 30;
+
+// Stored rows of a matrix and the byte extent of its storage.
+int64_t stored_rows(const scalify_scaled_array* x) { return x->trans ? x->cols : x->rows; }
+int64_t stored_cols(const scalify_scaled_array* x) { return x->trans ? x->rows : x->cols; }
+
+scalify_status check_matrix(const scalify_scaled_array* x, int64_t ld_multiple) {
+  if (x->rows < 0 || x->cols < 0 || x->rows > kMaxDim || x->cols > kMaxDim) return SCALIFY_ERR_SHAPE;
+  if (x->trans != 0 && x->trans != 1) return SCALIFY_ERR_LAYOUT;
+  if (x->rows == 0 || x->cols == 0) return SCALIFY_OK;
+  if (x->data == nullptr) return SCALIFY_ERR_NULL;
+  if (x->ld < stored_cols(x)) return SCALIFY_ERR_SHAPE;
+  if (x->ld % ld_multiple != 0 || !aligned16(x->data)) return SCALIFY_ERR_ALIGN;
+  return SCALIFY_OK;
+}
+
+size_t matmul_ws(int64_t M, int64_t N, int32_t out_dtype, int32_t rescale) {
+  if (M < 0 || N < 0 || !is_out(out_dtype) || (rescale != 0 && rescale != 1)) return 0;
+  return kHeaderBytes + (size_t)M * (size_t)round_up(N, 16) * (out_dtype == SCALIFY_F16 ? 4u : 2u);
+}
+
+scalify_status check_elementwise(const scalify_scaled_array* in, const scalify_scaled_array* out) {
+  if (!in || !out) return SCALIFY_ERR_NULL;
+  if (!out->scale) return SCALIFY_ERR_NULL;
+  if (!is_any(in->dtype) || !is_out(out->dtype)) return SCALIFY_ERR_DTYPE;
+  if (in->rows < 0 || in->cols < 0 || in->rows > kMaxDim || in->cols > kMaxDim) return SCALIFY_ERR_SHAPE;
+  if (in->rows != out->rows || in->cols != out->cols) return SCALIFY_ERR_SHAPE;
+  if (in->trans != out->trans || (in->trans != 0 && in->trans != 1)) return SCALIFY_ERR_LAYOUT;
+  const int64_t n = in->rows * in->cols;
+  if (n == 0) return SCALIFY_OK;
+  if (!in->data || !out->data) return SCALIFY_ERR_NULL;
+  if (in->ld != stored_cols(in) || out->ld != stored_cols(out)) return SCALIFY_ERR_LAYOUT;
+  if (!aligned16(in->data) || !aligned16(out->data)) return SCALIFY_ERR_ALIGN;
+  // Aliasing: allowed only as the very same buffer with the same element size.
+  const uintptr_t i0 = (uintptr_t)in->data, i1 = i0 + (uintptr_t)(n * elem_bytes(in->dtype));
+  const uintptr_t o0 = (uintptr_t)out->data, o1 = o0 + (uintptr_t)(n * elem_bytes(out->dtype));
+  if (i0 < o1 && o0 < i1 && !(i0 == o0 && elem_bytes(in->dtype) == elem_bytes(out->dtype)))
+    return SCALIFY_ERR_LAYOUT;
+  return SCALIFY_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t scalify_matmul_scale_log2(int64_t K) {
+  // Largest e with 2^e <= sqrt(K), i.e. 4^e <= K (integer arithmetic only).
+  int32_t e = 0;
+  if (K < 1) return 0;
+  while (e < 31 && ((int64_t)1 << (2 * (e + 1))) <= K) ++e;
+  return e;
+}
+
+size_t scalify_matmul_workspace_size(int64_t M, int64_t N, int32_t out_dtype, int32_t rescale) {
+  return matmul_ws(M, N, out_dtype, rescale);
+}
+
+size_t scalify_rescale_workspace_size(int64_t n) { return n < 0 ? 0 : kHeaderBytes; }
+
+const char* scalify_status_string(int32_t s) {
+  switch (s) {
+    case SCALIFY_OK: return "ok";
+    case SCALIFY_ERR_NULL: return "null pointer";
+    case SCALIFY_ERR_DTYPE: return "unsupported dtype";
+    case SCALIFY_ERR_SHAPE: return "bad shape";
+    case SCALIFY_ERR_LAYOUT: return "unsupported layout or aliasing";
+    case SCALIFY_ERR_ALIGN: return "misaligned pointer or leading dimension";
+    case SCALIFY_ERR_WORKSPACE: return "workspace missing or too small";
+    case SCALIFY_ERR_VALUE: return "scalar argument out of range";
+    case SCALIFY_ERR_HIP: return "HIP launch failed";
+    default: return "unknown status";
+  }
+}
+
+scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scaled_array* b,
+                              scalify_scaled_array* out, const scalify_matmul_opts* opts,
+                              void* workspace, size_t workspace_bytes, void* stream) {
+  if (!a || !b || !out || !opts) return SCALIFY_ERR_NULL;
+  if (!out->scale) return SCALIFY_ERR_NULL;
+  if (!is_fp8(a->dtype) || !is_fp8(b->dtype) || !is_out(opts->out_dtype) ||
+      out->dtype != opts->out_dtype)
+    return SCALIFY_ERR_DTYPE;
+  if (opts->rescale != SCALIFY_RESCALE_NONE && opts->rescale != SCALIFY_RESCALE_AMAX)
+    return SCALIFY_ERR_VALUE;
+  if (opts->target_log2 < -1000 || opts->target_log2 > 1000) return SCALIFY_ERR_VALUE;
+  if (out->trans != 0) return SCALIFY_ERR_LAYOUT;
+  const int64_t M = a->rows, K = a->cols, N = b->cols;
+  if (b->rows != K || out->rows != M || out->cols != N) return SCALIFY_ERR_SHAPE;
+  scalify_status st;
+  if ((st = check_matrix(a, 16)) != SCALIFY_OK) return st;
+  if ((st = check_matrix(b, 16)) != SCALIFY_OK) return st;
+  if ((st = check_matrix(out, out->dtype == SCALIFY_F16 ? 8 : 16)) != SCALIFY_OK) return st;
+  // 32-bit byte offsets inside the GEMM kernel.
+  if (M && K && stored_rows(a) * a->ld >= ((int64_t)1 << 32)) return SCALIFY_ERR_SHAPE;
+  if (K && N && stored_rows(b) * b->ld >= ((int64_t)1 << 32)) return SCALIFY_ERR_SHAPE;
+  const size_t need = matmul_ws(M, N, opts->out_dtype, opts->rescale);
+  if (!workspace || workspace_bytes < need || ((uintptr_t)workspace & 255u))
+    return SCALIFY_ERR_WORKSPACE;
+
+  hipStream_t s = (hipStream_t)stream;
+  uint32_t* hdr = (uint32_t*)workspace;
+  const int e_c = scalify_matmul_scale_log2(K);
+  const bool amax_mode = opts->rescale == SCALIFY_RESCALE_AMAX;
+  const int epi = opts->out_dtype == SCALIFY_F16 ? EPI_INTER32 : EPI_INTER16;
+
+  if (launch_prologue(hdr, a->scale, b->scale, s) != hipSuccess) return SCALIFY_ERR_HIP;
+
+  GemmParams p = {};
+  p.a = (const uint8_t*)a->data;
+  p.b = (const uint8_t*)b->data;
+  p.lda = a->ld;
+  p.ldb = b->ld;
+  p.M = (int)M;
+  p.N = (int)N;
+  p.K = (int)K;
+  p.tiles_m = (int)((M + 255) / 256);
+  p.tiles_n = (int)((N + 255) / 256);
+  p.a_bytes = (uint32_t)(stored_rows(a) * a->ld);
+  p.b_bytes = (uint32_t)(stored_rows(b) * b->ld);
+  p.e_c = e_c;
+  p.sat = opts->saturate != 0;
+  p.hdr = hdr;
+  p.inter = (uint8_t*)workspace + kHeaderBytes;
+  p.ldw = round_up(N, 16);
+  p.acc_out = opts->acc_out;
+  hipEvent_t* ev = (hipEvent_t*)opts->events;
+  if (ev && hipEventRecord(ev[0], s) != hipSuccess) return SCALIFY_ERR_HIP;
+  if (M > 0 && N > 0) {
+    if (launch_gemm(p, a->trans != 0, b->trans != 0, a->dtype, b->dtype, epi, s) != hipSuccess)
+      return SCALIFY_ERR_HIP;
+  }
+  if (ev && hipEventRecord(ev[1], s) != hipSuccess) return SCALIFY_ERR_HIP;
+  {
+    // Second pass: global amax -> rescale exponent -> output scale, and the
+    // cast of the intermediate (also for NONE mode, where e_r = 0).
+    EpilogueParams q = {};
+    q.inter = p.inter;
+    q.ldw = p.ldw;
+    q.out = out->data;
+    q.ldc = out->ld;
+    q.M = N > 0 ? (int)M : 0;
+    q.N = (int)N;
+    q.e_c = e_c;
+    q.target = opts->target_log2;
+    q.sat = p.sat;
+    q.mode = amax_mode ? 1 : 0;
+    q.hdr = hdr;
+    q.out_scale = out->scale;
+    q.amax_out = opts->amax_out;
+    if (launch_epilogue_cast(q, epi == EPI_INTER32, opts->out_dtype, s) != hipSuccess)
+      return SCALIFY_ERR_HIP;
+  }
+  if (ev && hipEventRecord(ev[2], s) != hipSuccess) return SCALIFY_ERR_HIP;
+  return SCALIFY_OK;
+}
+
+scalify_status scalify_rescale(const scalify_scaled_array* in, scalify_scaled_array* out,
+                               int32_t mode, int32_t target_log2, int32_t saturate,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+  scalify_status st = check_elementwise(in, out);
+  if (st != SCALIFY_OK) return st;
+  if (mode != SCALIFY_RESCALE_NONE && mode != SCALIFY_RESCALE_AMAX) return SCALIFY_ERR_VALUE;
+  if (target_log2 < -1000 || target_log2 > 1000) return SCALIFY_ERR_VALUE;
+  if (!workspace || workspace_bytes < kHeaderBytes || ((uintptr_t)workspace & 255u))
+    return SCALIFY_ERR_WORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  uint32_t* hdr = (uint32_t*)workspace;
+  const int64_t n = in->rows * in->cols;
+  if (launch_prologue(hdr, in->scale, nullptr, s) != hipSuccess) return SCALIFY_ERR_HIP;
+  if (mode == SCALIFY_RESCALE_AMAX && n > 0)
+    if (launch_amax(in->data, in->dtype, n, hdr, s) != hipSuccess) return SCALIFY_ERR_HIP;
+  ElemParams p = {};
+  p.in = in->data;
+  p.out = out->data;
+  p.n = n;
+  p.rule = mode == SCALIFY_RESCALE_AMAX ? RULE_AMAX : RULE_KEEP;
+  p.target = target_log2;
+  p.sat = saturate != 0;
+  p.hdr = hdr;
+  p.in_scale = in->scale;
+  p.out_scale = out->scale;
+  if (launch_elementwise(p, in->dtype, out->dtype, s) != hipSuccess) return SCALIFY_ERR_HIP;
+  return SCALIFY_OK;
+}
+
+scalify_status scalify_cast(const scalify_scaled_array* in, scalify_scaled_array* out,
+                            int32_t saturate, void* stream) {
+  scalify_status st = check_elementwise(in, out);
+  if (st != SCALIFY_OK) return st;
+  ElemParams p = {};
+  p.in = in->data;
+  p.out = out->data;
+  p.n = in->rows * in->cols;
+  p.rule = RULE_COPY;
+  p.sat = saturate != 0;
+  p.in_scale = in->scale;
+  p.out_scale = out->scale;
+  if (launch_elementwise(p, in->dtype, out->dtype, (hipStream_t)stream) != hipSuccess)
+    return SCALIFY_ERR_HIP;
+  return SCALIFY_OK;
+}
+
+scalify_status scalify_set_scaling(const scalify_scaled_array* in, scalify_scaled_array* out,
+                                   int32_t new_scale_log2, int32_t saturate, void* stream) {
+  scalify_status st = check_elementwise(in, out);
+  if (st != SCALIFY_OK) return st;
+  if (new_scale_log2 < -127 || new_scale_log2 > 127) return SCALIFY_ERR_VALUE;
+  if (in->scale != nullptr && in->scale == out->scale) return SCALIFY_ERR_LAYOUT;
+  ElemParams p = {};
+  p.in = in->data;
+  p.out = out->data;
+  p.n = in->rows * in->cols;
+  p.rule = RULE_FIXED;
+  p.e_fixed = new_scale_log2;
+  p.sat = saturate != 0;
+  p.in_scale = in->scale;
+  p.out_scale = out->scale;
+  if (launch_elementwise(p, in->dtype, out->dtype, (hipStream_t)stream) != hipSuccess)
+    return SCALIFY_ERR_HIP;
+  return SCALIFY_OK;
+}
+
+}  // extern "C"
