@@ -66,7 +66,7 @@ def _load():
     lib.or_matmul_acc.argtypes = [vp, c_int, c_int, c_i64, vp, c_int, c_int, c_i64,
                                   c_i64, c_i64, c_i64, vp]
     lib.or_matmul_acc_at.argtypes = [vp, c_int, c_int, c_i64, vp, c_int, c_int, c_i64,
-                                     c_i64, vp, vp, c_i64, vp, vp]
+                                     c_i64, vp, vp, c_i64, vp, vp, vp]
     lib.or_matmul_epilogue.argtypes = [vp, c_i64, c_f32, c_f32, c_i64, c_int, c_i32, c_int,
                                        c_int, vp, ctypes.POINTER(c_i32), ctypes.POINTER(c_f32)]
     lib.or_matmul_epilogue.restype = c_int
@@ -149,9 +149,10 @@ def matmul_acc(A: np.ndarray, fa: int, ta: bool, B: np.ndarray, fb: int, tb: boo
     return acc
 
 
-def matmul_acc_at(A, fa, ta, B, fb, tb, ii, jj):
-    """Accumulator at sampled output positions (ii[p], jj[p]) and the fp64
-    l2 norm of the product terms at each position."""
+def matmul_acc_at(A, fa, ta, B, fb, tb, ii, jj, l1=False):
+    """Accumulator at sampled output positions (ii[p], jj[p]) and a norm of
+    the product terms at each position: the l2 norm, or with l1=True the sum
+    of their magnitudes."""
     lib = _load()
     A, lda = _operand(A, ta)
     B, ldb = _operand(B, tb)
@@ -159,10 +160,11 @@ def matmul_acc_at(A, fa, ta, B, fb, tb, ii, jj):
     ii = np.ascontiguousarray(ii, dtype=np.int64)
     jj = np.ascontiguousarray(jj, dtype=np.int64)
     acc = np.empty(ii.shape, dtype=np.float32)
-    tn = np.empty(ii.shape, dtype=np.float64)
+    t2 = np.empty(ii.shape, dtype=np.float64)
+    t1 = np.empty(ii.shape, dtype=np.float64)
     lib.or_matmul_acc_at(_ptr(A), fa, int(ta), lda, _ptr(B), fb, int(tb), ldb, K,
-                         _ptr(ii), _ptr(jj), ii.size, _ptr(acc), _ptr(tn))
-    return acc, tn
+                         _ptr(ii), _ptr(jj), ii.size, _ptr(acc), _ptr(t2), _ptr(t1))
+    return acc, (t1 if l1 else t2)
 
 
 def matmul_epilogue(acc: np.ndarray, s_a: float, s_b: float, K: int, mode: int = RESCALE_AMAX,

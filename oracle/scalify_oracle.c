@@ -291,13 +291,14 @@ void or_matmul_acc(const uint8_t* A, int fa, int ta, int64_t lda,
     }
 }
 
-/* The same sum for a list of (i, j) pairs, plus the fp64 l2 norm of the
- * product terms sqrt(sum_k (a_ik b_kj)^2), which sets the accumulator
- * tolerance. */
+/* The same sum for a list of (i, j) pairs, plus two norms of the product
+ * terms that set the accumulator tolerance: l2 = sqrt(sum_k (a_ik b_kj)^2)
+ * and l1 = sum_k |a_ik b_kj| (the magnitude a dot product's rounding error
+ * is classically bounded against). Non-finite terms are left out of both. */
 void or_matmul_acc_at(const uint8_t* A, int fa, int ta, int64_t lda,
                       const uint8_t* B, int fb, int tb, int64_t ldb,
                       int64_t K, const int64_t* ii, const int64_t* jj, int64_t n,
-                      float* acc, double* term_norm)
+                      float* acc, double* term_l2, double* term_l1)
 {
     double da[256], db[256];
     int64_t p;
@@ -306,14 +307,15 @@ void or_matmul_acc_at(const uint8_t* A, int fa, int ta, int64_t lda,
     #pragma omp parallel for schedule(static)
     for (p = 0; p < n; ++p) {
         int64_t i = ii[p], j = jj[p], k;
-        double s = 0.0, q = 0.0;
+        double s = 0.0, q = 0.0, a1 = 0.0;
         for (k = 0; k < K; ++k) {
             double t = da[A_AT(i, k)] * db[B_AT(k, j)];
             s += t;
-            if (isfinite(t)) q += t * t;
+            if (isfinite(t)) { q += t * t; a1 += fabs(t); }
         }
         acc[p] = (float)s;
-        if (term_norm) term_norm[p] = sqrt(q);
+        if (term_l2) term_l2[p] = sqrt(q);
+        if (term_l1) term_l1[p] = a1;
     }
 }
 

@@ -289,10 +289,12 @@ def test_acc_at_matches_full_and_term_norm():
     ii = rng.integers(0, 40, 200)
     jj = rng.integers(0, 30, 200)
     acc, tn = orc.matmul_acc_at(A, orc.E4M3, False, B, orc.E5M2, False, ii, jj)
+    _, t1 = orc.matmul_acc_at(A, orc.E4M3, False, B, orc.E5M2, False, ii, jj, l1=True)
     assert np.array_equal(acc, full[ii, jj])
     dA, dB = torch_decode8(orc.E4M3, A), torch_decode8(orc.E5M2, B)
-    ref_tn = np.sqrt(((dA[ii, :] * dB[:, jj].T) ** 2).sum(axis=1))
-    assert np.allclose(tn, ref_tn, rtol=1e-12)
+    terms = dA[ii, :] * dB[:, jj].T
+    assert np.allclose(tn, np.sqrt((terms ** 2).sum(axis=1)), rtol=1e-12)
+    assert np.allclose(t1, np.abs(terms).sum(axis=1), rtol=1e-12)
 
 
 # ----------------------------------------------------------------------------- rescale / invariants
