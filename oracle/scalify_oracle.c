@@ -43,7 +43,7 @@ double or_decode_e4m3(uint32_t c)
 {
     int s = (c >> 7) & 1, e = (c >> 3) & 15, m = c & 7;
     double v;
-    if (e == 15 && m == 7) return NAN;
+    if (e == 15 && m == 7) return s ? -NAN : NAN;   /* the sign bit of a NaN is kept */
     if (e == 0) v = m * ldexp(1.0, -9);               /* subnormal: m/8 * 2^-6 */
     else v = (1.0 + m / 8.0) * ldexp(1.0, e - 7);
     return s ? -v : v;
@@ -54,7 +54,7 @@ double or_decode_e5m2(uint32_t c)
 {
     int s = (c >> 7) & 1, e = (c >> 2) & 31, m = c & 3;
     double v;
-    if (e == 31) return m ? NAN : (s ? -INFINITY : INFINITY);
+    if (e == 31) return m ? (s ? -NAN : NAN) : (s ? -INFINITY : INFINITY);
     if (e == 0) v = m * ldexp(1.0, -16);              /* subnormal: m/4 * 2^-14 */
     else v = (1.0 + m / 4.0) * ldexp(1.0, e - 15);
     return s ? -v : v;
@@ -65,7 +65,7 @@ double or_decode_f16(uint32_t h)
 {
     int s = (h >> 15) & 1, e = (h >> 10) & 31, m = h & 1023;
     double v;
-    if (e == 31) return m ? NAN : (s ? -INFINITY : INFINITY);
+    if (e == 31) return m ? (s ? -NAN : NAN) : (s ? -INFINITY : INFINITY);
     if (e == 0) v = m * ldexp(1.0, -24);
     else v = (1.0 + m / 1024.0) * ldexp(1.0, e - 15);
     return s ? -v : v;

@@ -425,3 +425,12 @@ def test_hand_derived_examples():
         assert acc.tolist() == case["acc"], case["name"]
         assert codes.tolist() == case["out_codes"], case["name"]
         assert e_out == case["out_scale_log2"], case["name"]
+
+
+def test_nan_sign_is_kept_through_decode_and_cast():
+    """Reading R7: a NaN keeps its sign bit (as torch's float8 casts do)."""
+    codes = np.array([0x7F, 0xFF], np.uint8)
+    assert list(orc.cast_data(codes, orc.E4M3, orc.E4M3)) == [0x7F, 0xFF]
+    assert list(orc.cast_data(codes, orc.E4M3, orc.F16)) == [0x7E00, 0xFE00]
+    ref = torch.from_numpy(np.array([np.nan, -np.nan], np.float32)).to(torch.float8_e4m3fn)
+    assert list(ref.view(torch.uint8).numpy()) == [0x7F, 0xFF]
