@@ -165,6 +165,9 @@ def scalify_matmul(a: ScaledArray, b: ScaledArray, out: ScaledArray, *, rescale:
         ws = workspace(scalify_matmul_workspace_size(M, N, out.fmt, rescale), a.data.device)
     ev_arr = None
     if events is not None:
+        for e in events:
+            if not e.cuda_event:       # torch creates its events lazily, on first record
+                e.record(stream if stream is not None else torch.cuda.current_stream())
         ev_arr = (ctypes.c_void_p * 3)(*[e.cuda_event for e in events])
     opts = CMatmulOpts(int(out.fmt), int(rescale), int(target_log2), int(bool(saturate)),
                        acc_out.data_ptr() if acc_out is not None else None,
