@@ -106,31 +106,31 @@ __global__ __launch_bounds__(EW_THREADS) void epilogue_cast_kernel(EpilogueParam
   const int e_out = clamp_e8m0(e_ab + p.e_c + e_r);
   const int shift = e_out - e_ab;  // data' = acc * 2^-shift
   const bool sat = p.sat != 0;
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
+  if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) {
     *p.out_scale = pow2_float(e_out);
     if (p.amax_out) *p.amax_out = __uint_as_float(amax_raw) * pow2_float(-p.e_c);
   }
-  const int64_t cpr = (p.N + 15) / 16;
-  const int64_t total = (int64_t)p.M * cpr;
-  for (int64_t idx = (int64_t)blockIdx.x * EW_THREADS + threadIdx.x; idx < total;
-       idx += (int64_t)gridDim.x * EW_THREADS) {
-    const int64_t m = idx / cpr;
-    const int n = (int)(idx - m * cpr) * 16;
-    uint32_t c[16];
-    if (INTER32) {
-      load16<kF32>(p.inter, m * p.ldw + n, c);
-    } else {
-      load16<kF16>(p.inter, m * p.ldw + n, c);  // 16-bit containers
+  // 2-D grid: blockIdx.y walks rows, x-threads walk 16-element chunks.
+  const int cpr = (p.N + 15) / 16;
+  for (int m = blockIdx.y; m < p.M; m += gridDim.y) {
+    for (int ch = blockIdx.x * EW_THREADS + threadIdx.x; ch < cpr; ch += gridDim.x * EW_THREADS) {
+      const int n = ch * 16;
+      uint32_t c[16];
+      if (INTER32) {
+        load16<kF32>(p.inter, (int64_t)m * p.ldw + n, c);
+      } else {
+        load16<kF16>(p.inter, (int64_t)m * p.ldw + n, c);  // 16-bit containers
 #pragma unroll
-      for (int i = 0; i < 16; ++i) c[i] <<= 16;
-    }
+        for (int i = 0; i < 16; ++i) c[i] <<= 16;
+      }
 #pragma unroll
-    for (int i = 0; i < 16; ++i) c[i] = cast_bits<OUTF>(c[i], shift, sat);
-    if (n + 16 <= p.N) {
-      store16<OUTF>(p.out, m * p.ldc + n, c);
-    } else {
-      for (int i = 0; i < 16; ++i)
-        if (n + i < p.N) store1<OUTF>(p.out, m * p.ldc + n + i, c[i]);
+      for (int i = 0; i < 16; ++i) c[i] = cast_bits<OUTF>(c[i], shift, sat);
+      if (n + 16 <= p.N) {
+        store16<OUTF>(p.out, (int64_t)m * p.ldc + n, c);
+      } else {
+        for (int i = 0; i < 16; ++i)
+          if (n + i < p.N) store1<OUTF>(p.out, (int64_t)m * p.ldc + n + i, c[i]);
+      }
     }
   }
 }
@@ -144,8 +144,10 @@ static int grid_for(int64_t work) {
 
 hipError_t launch_epilogue_cast(const EpilogueParams& p, int inter32, int out_dtype,
                                 hipStream_t s) {
-  const int grid = grid_for((int64_t)p.M * ((p.N + 15) / 16));
-  const dim3 g(grid), b(EW_THREADS);
+  const int cpr = (p.N + 15) / 16;
+  const int gx = (cpr + EW_THREADS - 1) / EW_THREADS;
+  const int gy = p.M < 1 ? 1 : (p.M > 65535 ? 65535 : p.M);
+  const dim3 g(gx < 1 ? 1 : gx, gy), b(EW_THREADS);
   if (inter32) {
     hipLaunchKernelGGL((epilogue_cast_kernel<1, kF16>), g, b, 0, s, p);
   } else if (out_dtype == kE4M3) {

@@ -5,9 +5,12 @@
 // (Section 3.3) and a compact pre-cast intermediate for the cast kernel
 // that follows (the rescale exponent needs the amax of the whole output).
 //
-// Design (per workgroup of 256 threads = 4 wave64):
+// Design (per workgroup of 512 threads = 8 wave64, two per SIMD):
 //   * 256 x 256 output tile, K consumed in 128-byte steps; each wave owns a
-//     128 x 128 quadrant = 8 x 8 tiles of v_mfma_f32_16x16x128_f8f6f4.
+//     64 x 128 sub-tile = 4 x 8 tiles of v_mfma_f32_16x16x128_f8f6f4, with
+//     the accumulators in registers; the two waves of a SIMD cover each
+//     other's LDS waits, and within a wave the next B fragment is read while
+//     the current MFMAs issue.
 //   * A and B k-slices (32 KiB each) stream HBM -> LDS with
 //     global_load_lds_dwordx4 (16 B per lane, no VGPR staging), double
 //     buffered: 4 x 32 KiB = 128 KiB of the 160 KiB LDS.
@@ -40,7 +43,13 @@ typedef int v2i __attribute__((ext_vector_type(2)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 #define LDS_AS __attribute__((address_space(3)))
 
-constexpr int BM = 256, BN = 256, BK = 128, NTHR = 256;
+constexpr int BM = 256, BN = 256, BK = 128;
+// 8 waves (2 per SIMD, so one wave's LDS waits overlap the other's MFMAs),
+// arranged 4 along M x 2 along N; each owns a 64 x 128 sub-tile.
+constexpr int WAVES = 8, WAVES_N = 2, WAVES_M = WAVES / WAVES_N, NTHR = 64 * WAVES;
+constexpr int WTM = BM / WAVES_M, WTN = BN / WAVES_N;      // 64 x 128
+constexpr int MI = WTM / 16, NI = WTN / 16;                // 4 x 8 MFMA tiles
+constexpr int BPW = 32 / WAVES;                            // 1 KiB load blocks per wave and operand
 constexpr int TILE_BYTES = 32768;
 
 // 16-byte chunk swizzles (see file comment). KC: 16 consecutive rows read
@@ -98,6 +107,7 @@ struct TileLoader {
 template <bool KC>
 __device__ __forceinline__ TileLoader make_loader(uint32_t ld, int wave, int lane) {
   TileLoader L;
+  const int hi = ((wave * BPW) >> 3) & 1;  // bit 5 of the k-rows this wave loads (MC)
 #pragma unroll
   for (int par = 0; par < 2; ++par) {
     if (KC) {
@@ -105,7 +115,7 @@ __device__ __forceinline__ TileLoader make_loader(uint32_t ld, int wave, int lan
       L.lane_off[par] = (uint32_t)(lane >> 3) * ld + 16u * (uint32_t)c;
       L.kchunk[par] = 16 * c;
     } else {
-      const int c = (lane & 15) ^ (par * 4 + (lane >> 4)) ^ ((wave & 1) << 3);
+      const int c = (lane & 15) ^ (par * 4 + (lane >> 4)) ^ (hi << 3);
       L.lane_off[par] = (uint32_t)(lane >> 4) * ld + 16u * (uint32_t)c;
       L.kchunk[par] = 0;
     }
@@ -123,8 +133,8 @@ __device__ __forceinline__ void issue_tile(v4i rsrc, const TileLoader& L, uint32
                                            int k0, int K, uint8_t* lds, int wave) {
   const uint32_t oob = (uint32_t)rsrc.z;
 #pragma unroll
-  for (int q = 0; q < 8; ++q) {
-    const int blk = wave * 8 + q;
+  for (int q = 0; q < BPW; ++q) {
+    const int blk = wave * BPW + q;
     uint32_t off;
     if (KC) {
       off = (uint32_t)(row0 + blk * 8) * ld + (uint32_t)k0 + L.lane_off[q & 1];
@@ -139,7 +149,8 @@ __device__ __forceinline__ void issue_tile(v4i rsrc, const TileLoader& L, uint32
 // KC tiles when K is not a multiple of 16: zero the bytes k >= krem of the
 // chunk that straddles K (chunks wholly beyond K were loaded as zeros).
 __device__ __forceinline__ void zero_tail_kc(uint8_t* lds, int krem, int tid) {
-  const int r = tid;  // 256 rows, one per thread
+  const int r = tid;  // 256 rows, one per thread (threads >= 256 idle)
+  if (r >= 256) return;
   const int c = krem >> 4;
   uint8_t* chunk = lds + r * 128 + ((c ^ swz_kc(r)) * 16);
   for (int b = krem & 15; b < 16; ++b) chunk[b] = 0;
@@ -189,16 +200,36 @@ __device__ __forceinline__ void static_for(F&& f) {
 }
 
 template <bool A_MN, bool B_KC, int FA, int FB>
-__device__ __forceinline__ void mma_step(v4f (&acc)[8][8], const uint8_t* cA, const uint8_t* cB,
+__device__ __forceinline__ void mma_step(v4f (&acc)[MI][NI], const uint8_t* cA, const uint8_t* cB,
                                          int wm, int wn, int lane) {
-  v8i af[8];
+  // All A fragments of the sub-tile, then the B fragments one 16-column
+  // group at a time; the next group's fragment is read while the current
+  // group's MFMAs issue (the schedule below interleaves them one by one),
+  // so its LDS latency is hidden behind matrix work.
+  constexpr int DSA = A_MN ? 4 : 2;  // LDS reads per A fragment
+  constexpr int DSB = B_KC ? 2 : 4;  // LDS reads per B fragment
+  v8i af[MI];
 #pragma unroll
-  for (int mi = 0; mi < 8; ++mi) af[mi] = read_frag<!A_MN>(cA, wm + 16 * mi, lane);
+  for (int mi = 0; mi < MI; ++mi) af[mi] = read_frag<!A_MN>(cA, wm + 16 * mi, lane);
+  v8i bf = read_frag<B_KC>(cB, wn, lane);
 #pragma unroll
-  for (int ni = 0; ni < 8; ++ni) {
-    const v8i bf = read_frag<B_KC>(cB, wn + 16 * ni, lane);
+  for (int ni = 0; ni < NI; ++ni) {
+    v8i bn;
+    if (ni + 1 < NI) bn = read_frag<B_KC>(cB, wn + 16 * (ni + 1), lane);
 #pragma unroll
-    for (int mi = 0; mi < 8; ++mi) acc[mi][ni] = mfma<FA, FB>(bf, af[mi], acc[mi][ni]);
+    for (int mi = 0; mi < MI; ++mi) acc[mi][ni] = mfma<FA, FB>(bf, af[mi], acc[mi][ni]);
+    if (ni + 1 < NI) bf = bn;
+  }
+  // Instruction order: first fragments, then per group MFMA / LDS-read pairs.
+  __builtin_amdgcn_sched_group_barrier(0x100, MI * DSA + DSB, 0);
+#pragma unroll
+  for (int ni = 0; ni < NI; ++ni) {
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      if (ni + 1 < NI && mi < DSB) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    if (ni + 1 < NI && DSB > MI) __builtin_amdgcn_sched_group_barrier(0x100, DSB - MI, 0);
   }
 }
 
@@ -208,7 +239,7 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
   __shared__ __attribute__((aligned(1024))) uint8_t sB0[TILE_BYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t sA1[TILE_BYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t sB1[TILE_BYTES];
-  __shared__ float red[4];
+  __shared__ float red[WAVES];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -256,14 +287,14 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
     }
   };
 
-  v4f acc[8][8];
+  v4f acc[MI][NI];
 #pragma unroll
-  for (int i = 0; i < 8; ++i)
+  for (int i = 0; i < MI; ++i)
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < NI; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
 
-  const int wm = (wave >> 1) * 128;  // wave quadrant
-  const int wn = (wave & 1) * 128;
+  const int wm = (wave / WAVES_N) * WTM;  // wave sub-tile
+  const int wn = (wave % WAVES_N) * WTN;
 
   if (KT > 0) issue(0, sA0, sB0);
   for (int kt = 0; kt < KT; ++kt) {
@@ -281,8 +312,8 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
   float lmax = 0.f;
   const int mb = m0 + wm + (lane & 15);
   const int nb = n0 + wn + 4 * (lane >> 4);
-  static_for<0, 64>([&](auto I) {
-    constexpr int mi = decltype(I)::value / 8, ni = decltype(I)::value % 8;
+  static_for<0, MI * NI>([&](auto I) {
+    constexpr int mi = decltype(I)::value / NI, ni = decltype(I)::value % NI;
     const int m = mb + 16 * mi;
     const int n = nb + 16 * ni;
     const v4f v = acc[mi][ni];
@@ -316,7 +347,8 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
   if (lane == 0) red[wave] = lmax;
   __syncthreads();
   if (tid == 0) {
-    const float wmax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    float wmax = red[0];
+    for (int w = 1; w < WAVES; ++w) wmax = fmaxf(wmax, red[w]);
     atomicMax(p.hdr, __float_as_uint(wmax));
   }
 }

@@ -110,9 +110,10 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
   if ((st = check_matrix(a, 16)) != SCALIFY_OK) return st;
   if ((st = check_matrix(b, 16)) != SCALIFY_OK) return st;
   if ((st = check_matrix(out, out->dtype == SCALIFY_F16 ? 8 : 16)) != SCALIFY_OK) return st;
-  // 32-bit byte offsets inside the GEMM kernel.
-  if (M && K && stored_rows(a) * a->ld >= ((int64_t)1 << 32)) return SCALIFY_ERR_SHAPE;
-  if (K && N && stored_rows(b) * b->ld >= ((int64_t)1 << 32)) return SCALIFY_ERR_SHAPE;
+  // 32-bit byte offsets inside the GEMM kernel, including the range-checked
+  // reads of up to one tile past the last stored row.
+  if (M && K && (stored_rows(a) + 256) * a->ld + 256 >= ((int64_t)1 << 32)) return SCALIFY_ERR_SHAPE;
+  if (K && N && (stored_rows(b) + 256) * b->ld + 256 >= ((int64_t)1 << 32)) return SCALIFY_ERR_SHAPE;
   const size_t need = matmul_ws(M, N, opts->out_dtype, opts->rescale);
   if (!workspace || workspace_bytes < need || ((uintptr_t)workspace & 255u))
     return SCALIFY_ERR_WORKSPACE;
