@@ -105,6 +105,55 @@ __device__ __forceinline__ uint32_t cast_bits(uint32_t u, int shift, bool sat) {
   return mag | sign;
 }
 
+// ---------------------------------------------------------------------------
+// Fast path: the gfx950 conversion v_cvt_scalef32_pk_{fp8,bf8}_f32 computes
+// round-to-nearest-even of x / scale into OCP E4M3 / E5M2 with the
+// non-saturating overflow rule (E4M3 -> NaN code, E5M2 -> Inf code). With
+// scale = 2^shift this is exactly cast_bits(u, shift, sat = false) for every
+// non-NaN fp32 input (checked against cast_bits on a structured sweep of
+// exponents, mantissa tie and sticky patterns, specials and random inputs,
+// shifts -60..60). NaN inputs are not handled here: callers route chunks
+// that contain a NaN to cast_bits.
+
+typedef short v2s_t __attribute__((ext_vector_type(2)));
+
+// Largest |shift| for which 2^shift is a normal fp32.
+constexpr int kFastShiftMax = 126;
+
+// Saturation fix-up on 4 packed codes: overflow codes -> +-max (same sign).
+// E4M3 overflow is 0x7F|s (max 0x7E|s); E5M2 overflow is 0x7C|s (0x7B|s):
+// subtract one in exactly the bytes whose low 7 bits equal the overflow code.
+template <int F>
+__device__ __forceinline__ uint32_t saturate4(uint32_t w) {
+  const uint32_t low = w & 0x7F7F7F7Fu;
+  uint32_t hit;
+  if (F == kE4M3) {
+    hit = (low + 0x01010101u) & 0x80808080u;  // 0x7F + 1 carries into bit 7
+  } else {
+    const uint32_t x = low ^ 0x7C7C7C7Cu;     // zero byte where low == 0x7C
+    hit = (x - 0x01010101u) & ~x & 0x80808080u;
+  }
+  return w - (hit >> 7);
+}
+
+// 4 non-NaN fp32 values (bits) times 2^-shift -> 4 packed FP8 codes.
+template <int F>
+__device__ __forceinline__ uint32_t cast4_fp8_hw(uint32_t u0, uint32_t u1, uint32_t u2, uint32_t u3,
+                                                 float scale, bool sat) {
+  v2s_t r = {0, 0};
+  if (F == kE4M3) {
+    r = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(r, __uint_as_float(u0), __uint_as_float(u1), scale, false);
+    r = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(r, __uint_as_float(u2), __uint_as_float(u3), scale, true);
+  } else {
+    r = __builtin_amdgcn_cvt_scalef32_pk_bf8_f32(r, __uint_as_float(u0), __uint_as_float(u1), scale, false);
+    r = __builtin_amdgcn_cvt_scalef32_pk_bf8_f32(r, __uint_as_float(u2), __uint_as_float(u3), scale, true);
+  }
+  const uint32_t w = __builtin_bit_cast(uint32_t, r);
+  return sat ? saturate4<F>(w) : w;
+}
+
+__device__ __forceinline__ bool is_nan_bits(uint32_t u) { return (u & 0x7FFFFFFFu) > 0x7F800000u; }
+
 // Exact fp32 bits of an FP8 / FP16 code (all FP8 and FP16 values are fp32).
 template <int F>
 __device__ __forceinline__ uint32_t decode_bits(uint32_t c);

@@ -68,7 +68,6 @@ __device__ __forceinline__ uint32_t to_bits(uint32_t c) {
   else return decode_bits<F>(c);
 }
 
-// Store 16 codes of output format F (FP8: 16 B, FP16: 32 B).
 template <int F>
 __device__ __forceinline__ void store16(void* base, int64_t e, const uint32_t (&c)[16]) {
   if (F == kF16) {
@@ -94,6 +93,52 @@ __device__ __forceinline__ void store1(void* base, int64_t e, uint32_t c) {
   else ((uint8_t*)base)[e] = (uint8_t)c;
 }
 
+// 16 fp32 values (bits) times 2^-shift -> 16 codes packed in 4 words (FP8)
+// or 8 words (FP16: two codes per word). FP8 uses the hardware conversion
+// when the scale fits and no value is NaN, else the integer cast.
+template <int OUTF>
+__device__ __forceinline__ void encode16(const uint32_t (&u)[16], int shift, float scale, bool fast,
+                                         bool sat, uint32_t (&w)[8]) {
+  if (OUTF == kE4M3 || OUTF == kE5M2) {
+    bool nan = false;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) nan |= is_nan_bits(u[i]);
+    if (fast && !nan) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        w[q] = cast4_fp8_hw<OUTF>(u[4 * q], u[4 * q + 1], u[4 * q + 2], u[4 * q + 3], scale, sat);
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        w[q] = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) w[q] |= cast_bits<OUTF>(u[4 * q + i], shift, sat) << (8 * i);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+      w[q] = cast_bits<OUTF>(u[2 * q], shift, sat) | (cast_bits<OUTF>(u[2 * q + 1], shift, sat) << 16);
+  }
+}
+
+template <int OUTF>
+__device__ __forceinline__ void store_words16(void* base, int64_t e, const uint32_t (&w)[8]) {
+  if (OUTF == kF16) {
+    *(u4*)((uint16_t*)base + e) = u4{w[0], w[1], w[2], w[3]};
+    *(u4*)((uint16_t*)base + e + 8) = u4{w[4], w[5], w[6], w[7]};
+  } else {
+    *(u4*)((uint8_t*)base + e) = u4{w[0], w[1], w[2], w[3]};
+  }
+}
+
+// Element i of the packed words.
+template <int OUTF>
+__device__ __forceinline__ uint32_t word_code(const uint32_t (&w)[8], int i) {
+  if (OUTF == kF16) return (w[i >> 1] >> (16 * (i & 1))) & 0xFFFFu;
+  return (w[i >> 2] >> (8 * (i & 3))) & 0xFFu;
+}
+
 // ---------------------------------------------------------------- GEMM epilogue cast
 
 template <int INTER32, int OUTF>
@@ -106,6 +151,8 @@ __global__ __launch_bounds__(EW_THREADS) void epilogue_cast_kernel(EpilogueParam
   const int e_out = clamp_e8m0(e_ab + p.e_c + e_r);
   const int shift = e_out - e_ab;  // data' = acc * 2^-shift
   const bool sat = p.sat != 0;
+  const bool fast = shift >= -kFastShiftMax && shift <= kFastShiftMax;
+  const float scale = fast ? pow2_float(shift) : 1.0f;
   if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) {
     *p.out_scale = pow2_float(e_out);
     if (p.amax_out) *p.amax_out = __uint_as_float(amax_raw) * pow2_float(-p.e_c);
@@ -123,13 +170,13 @@ __global__ __launch_bounds__(EW_THREADS) void epilogue_cast_kernel(EpilogueParam
 #pragma unroll
         for (int i = 0; i < 16; ++i) c[i] <<= 16;
       }
-#pragma unroll
-      for (int i = 0; i < 16; ++i) c[i] = cast_bits<OUTF>(c[i], shift, sat);
+      uint32_t w[8];
+      encode16<OUTF>(c, shift, scale, fast, sat, w);
       if (n + 16 <= p.N) {
-        store16<OUTF>(p.out, (int64_t)m * p.ldc + n, c);
+        store_words16<OUTF>(p.out, (int64_t)m * p.ldc + n, w);
       } else {
         for (int i = 0; i < 16; ++i)
-          if (n + i < p.N) store1<OUTF>(p.out, (int64_t)m * p.ldc + n + i, c[i]);
+          if (n + i < p.N) store1<OUTF>(p.out, (int64_t)m * p.ldc + n + i, word_code<OUTF>(w, i));
       }
     }
   }
@@ -210,6 +257,8 @@ __global__ __launch_bounds__(EW_THREADS) void elementwise_kernel(ElemParams p) {
     shift = e_out - e_in;
   }
   const bool sat = p.sat != 0;
+  const bool fast = shift >= -kFastShiftMax && shift <= kFastShiftMax;
+  const float scale = fast ? pow2_float(shift) : 1.0f;
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     if (p.rule == RULE_COPY) *p.out_scale = p.in_scale ? *p.in_scale : 1.0f;
     else *p.out_scale = pow2_float(e_out);
@@ -220,8 +269,10 @@ __global__ __launch_bounds__(EW_THREADS) void elementwise_kernel(ElemParams p) {
     uint32_t c[16];
     load16<INF>(p.in, v * 16, c);
 #pragma unroll
-    for (int i = 0; i < 16; ++i) c[i] = cast_bits<OUTF>(to_bits<INF>(c[i]), shift, sat);
-    store16<OUTF>(p.out, v * 16, c);
+    for (int i = 0; i < 16; ++i) c[i] = to_bits<INF>(c[i]);
+    uint32_t w[8];
+    encode16<OUTF>(c, shift, scale, fast, sat, w);
+    store_words16<OUTF>(p.out, v * 16, w);
   }
   if (blockIdx.x == 0)
     for (int64_t e = nv * 16 + threadIdx.x; e < p.n; e += EW_THREADS)
