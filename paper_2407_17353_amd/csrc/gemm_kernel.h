@@ -7,13 +7,21 @@
 //
 // Design (per workgroup of 512 threads = 8 wave64, two per SIMD):
 //   * 256 x 256 output tile, K consumed in 128-byte steps; each wave owns a
-//     64 x 128 sub-tile = 4 x 8 tiles of v_mfma_f32_16x16x128_f8f6f4, with
+//     64 x 128 sub-tile = 4 x 8 tiles of v_mfma_f32_16x16x128_f8f6f4 with
 //     the accumulators in registers; the two waves of a SIMD cover each
-//     other's LDS waits, and within a wave the next B fragment is read while
-//     the current MFMAs issue.
-//   * A and B k-slices (32 KiB each) stream HBM -> LDS with
-//     global_load_lds_dwordx4 (16 B per lane, no VGPR staging), double
-//     buffered: 4 x 32 KiB = 128 KiB of the 160 KiB LDS.
+//     other's waits.
+//   * A and B k-slices (32 KiB each per step) stream HBM -> LDS with
+//     buffer_load_dwordx4 ... lds (16 B per lane, no VGPR staging) into two
+//     64 KiB stages. Buffer loads are range-checked: rows past the matrix,
+//     and K past its end, read as zeros without touching memory.
+//   * Software pipeline with one barrier per step, placed before the last
+//     quarter of the step's MFMAs: by then every wave holds the B fragments
+//     it still needs, so after the barrier the step's stage is free and
+//     the loads of step s + 2 are issued into it, two per row block of
+//     MFMAs; in the same stretch each wave refills its A fragments with
+//     those of step s + 1 (landed before the barrier) as soon as their last
+//     MFMA has issued. MFMAs never wait for a barrier-to-first-fragment
+//     round trip, and loads have a whole step to land.
 //   * Operands whose K is contiguous in memory ("KC" tiles, 128 B rows) are
 //     read with ds_read_b128; operands whose M or N is contiguous ("MC"
 //     tiles, 256 B rows along k) are read with ds_read_b64_tr_b8, which
@@ -21,9 +29,10 @@
 //     feeds the MFMA without a separate transpose pass.
 //   * Both tile kinds are XOR-swizzled in 16-byte chunks so that fragment
 //     reads hit distinct LDS banks; the swizzle is applied on the global
-//     side of the loads because global_load_lds writes lane i at base+16*i.
+//     side of the loads because the LDS-direct load writes lane i at
+//     M0 + 16 i.
 //   * The MFMA is issued with B as its first operand, so each lane ends up
-//     holding 4 consecutive output columns: the epilogue stores 4/8/16-byte
+//     holding 4 consecutive output columns: the epilogue stores 8 or 16 byte
 //     vectors per lane without an LDS round trip.
 //   * Tile order: workgroup ids are remapped so that each XCD (ids are
 //     dealt round-robin over the 8 XCDs) walks a contiguous range of tiles,
@@ -44,13 +53,13 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 #define LDS_AS __attribute__((address_space(3)))
 
 constexpr int BM = 256, BN = 256, BK = 128;
-// 8 waves (2 per SIMD, so one wave's LDS waits overlap the other's MFMAs),
-// arranged 4 along M x 2 along N; each owns a 64 x 128 sub-tile.
+// 8 waves (two per SIMD) arranged 4 x 2; each owns a 64 x 128 sub-tile.
 constexpr int WAVES = 8, WAVES_N = 2, WAVES_M = WAVES / WAVES_N, NTHR = 64 * WAVES;
 constexpr int WTM = BM / WAVES_M, WTN = BN / WAVES_N;      // 64 x 128
 constexpr int MI = WTM / 16, NI = WTN / 16;                // 4 x 8 MFMA tiles
 constexpr int BPW = 32 / WAVES;                            // 1 KiB load blocks per wave and operand
 constexpr int TILE_BYTES = 32768;
+constexpr int LOADS_PER_STEP = 2 * BPW;                    // load instructions per wave and step
 
 // 16-byte chunk swizzles (see file comment). KC: 16 consecutive rows read
 // the same logical chunk from 16 distinct bank groups. MC: the 8 rows a
@@ -76,8 +85,8 @@ __device__ __forceinline__ v4i make_rsrc(const void* base, uint32_t bytes) {
 // M0 has no other user in these kernels (no LDS-DMA builtins, no indexed
 // register moves), so clobbering it here is safe.
 // Issued as inline asm so that the compiler does not order every later LDS
-// read behind it; completion is awaited explicitly (s_waitcnt vmcnt(0))
-// before the barrier that publishes a k-step.
+// read behind it; completion is awaited explicitly (wait_vmcnt) before the
+// barrier that publishes a k-step.
 __device__ __forceinline__ void load_lds16(v4i rsrc, uint32_t voff, uint8_t* lds_base) {
   const uint32_t lds_addr = (uint32_t)(uintptr_t)(LDS_AS void*)lds_base;
 #pragma clang diagnostic push
@@ -89,6 +98,14 @@ __device__ __forceinline__ void load_lds16(v4i rsrc, uint32_t voff, uint8_t* lds
       : "s"(lds_addr), "v"(voff), "s"(rsrc)
       : "memory", "m0");
 #pragma clang diagnostic pop
+}
+
+// Wait until at most N of this wave's vector memory loads are outstanding
+// (they complete in issue order).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
 // Per-thread parts of the chunk offsets of one operand tile. Lane i of a
@@ -123,27 +140,24 @@ __device__ __forceinline__ TileLoader make_loader(uint32_t ld, int wave, int lan
   return L;
 }
 
-// Issue the 8 chunk loads (1 KiB per wave instruction) of one operand tile
-// for the k-step starting at k0. Out-of-matrix rows (beyond M or N for KC,
-// beyond K for MC) read zeros through the buffer range check; in the
-// partial last k-step (TAIL) KC chunks that start at or beyond K are sent
-// out of range too, and a chunk straddling K is trimmed by zero_tail.
-template <bool KC, bool TAIL>
-__device__ __forceinline__ void issue_tile(v4i rsrc, const TileLoader& L, uint32_t ld, int row0,
-                                           int k0, int K, uint8_t* lds, int wave) {
-  const uint32_t oob = (uint32_t)rsrc.z;
-#pragma unroll
-  for (int q = 0; q < BPW; ++q) {
-    const int blk = wave * BPW + q;
-    uint32_t off;
-    if (KC) {
-      off = (uint32_t)(row0 + blk * 8) * ld + (uint32_t)k0 + L.lane_off[q & 1];
-      if (TAIL && k0 + L.kchunk[q & 1] >= K) off = oob;
-    } else {
-      off = (uint32_t)(k0 + blk * 4) * ld + (uint32_t)row0 + L.lane_off[q & 1];
-    }
-    load_lds16(rsrc, off, lds + blk * 1024);
+// Issue chunk load q (0 .. BPW - 1; 1 KiB per wave instruction) of this
+// wave's share of one operand tile for the k-step starting at k0.
+// Out-of-matrix rows (beyond M or N for KC, beyond K for MC) read zeros
+// through the buffer range check; KC chunks that start at or beyond K are
+// sent out of range too, and a chunk straddling K is trimmed by
+// zero_tail_kc.
+template <bool KC>
+__device__ __forceinline__ void issue_block(v4i rsrc, const TileLoader& L, uint32_t ld, int row0,
+                                            int k0, int K, uint8_t* lds, int wave, int q) {
+  const int blk = wave * BPW + q;
+  uint32_t off;
+  if (KC) {
+    off = (uint32_t)(row0 + blk * 8) * ld + (uint32_t)k0 + L.lane_off[q & 1];
+    if (k0 + L.kchunk[q & 1] >= K) off = (uint32_t)rsrc.z;
+  } else {
+    off = (uint32_t)(k0 + blk * 4) * ld + (uint32_t)row0 + L.lane_off[q & 1];
   }
+  load_lds16(rsrc, off, lds + blk * 1024);
 }
 
 // KC tiles when K is not a multiple of 16: zero the bytes k >= krem of the
@@ -199,40 +213,6 @@ __device__ __forceinline__ void static_for(F&& f) {
   }
 }
 
-template <bool A_MN, bool B_KC, int FA, int FB>
-__device__ __forceinline__ void mma_step(v4f (&acc)[MI][NI], const uint8_t* cA, const uint8_t* cB,
-                                         int wm, int wn, int lane) {
-  // All A fragments of the sub-tile, then the B fragments one 16-column
-  // group at a time; the next group's fragment is read while the current
-  // group's MFMAs issue (the schedule below interleaves them one by one),
-  // so its LDS latency is hidden behind matrix work.
-  constexpr int DSA = A_MN ? 4 : 2;  // LDS reads per A fragment
-  constexpr int DSB = B_KC ? 2 : 4;  // LDS reads per B fragment
-  v8i af[MI];
-#pragma unroll
-  for (int mi = 0; mi < MI; ++mi) af[mi] = read_frag<!A_MN>(cA, wm + 16 * mi, lane);
-  v8i bf = read_frag<B_KC>(cB, wn, lane);
-#pragma unroll
-  for (int ni = 0; ni < NI; ++ni) {
-    v8i bn;
-    if (ni + 1 < NI) bn = read_frag<B_KC>(cB, wn + 16 * (ni + 1), lane);
-#pragma unroll
-    for (int mi = 0; mi < MI; ++mi) acc[mi][ni] = mfma<FA, FB>(bf, af[mi], acc[mi][ni]);
-    if (ni + 1 < NI) bf = bn;
-  }
-  // Instruction order: first fragments, then per group MFMA / LDS-read pairs.
-  __builtin_amdgcn_sched_group_barrier(0x100, MI * DSA + DSB, 0);
-#pragma unroll
-  for (int ni = 0; ni < NI; ++ni) {
-#pragma unroll
-    for (int mi = 0; mi < MI; ++mi) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      if (ni + 1 < NI && mi < DSB) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    }
-    if (ni + 1 < NI && DSB > MI) __builtin_amdgcn_sched_group_barrier(0x100, DSB - MI, 0);
-  }
-}
-
 template <bool A_MN, bool B_KC, int FA, int FB, int EPI>
 __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
   __shared__ __attribute__((aligned(1024))) uint8_t sA0[TILE_BYTES];
@@ -270,21 +250,22 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
   const TileLoader la = make_loader<!A_MN>(lda, wave, lane);
   const TileLoader lb = make_loader<B_KC>(ldb, wave, lane);
 
-  auto issue = [&](int kt, uint8_t* dA, uint8_t* dB) {
-    if (kt < KT_full) {
-      issue_tile<!A_MN, false>(ra, la, lda, m0, kt * BK, K, dA, wave);
-      issue_tile<B_KC, false>(rb, lb, ldb, n0, kt * BK, K, dB, wave);
-    } else {
-      issue_tile<!A_MN, true>(ra, la, lda, m0, kt * BK, K, dA, wave);
-      issue_tile<B_KC, true>(rb, lb, ldb, n0, kt * BK, K, dB, wave);
-    }
+  // Load j of a step: j < BPW are A blocks, the rest B blocks.
+  auto issue_one = [&](int j, int kt, uint8_t* dA, uint8_t* dB) {
+    if (j < BPW)
+      issue_block<!A_MN>(ra, la, lda, m0, kt * BK, K, dA, wave, j);
+    else
+      issue_block<B_KC>(rb, lb, ldb, n0, kt * BK, K, dB, wave, j - BPW);
   };
-  auto fix_tail = [&](int kt, uint8_t* dA, uint8_t* dB) {
-    if (kt == KT_full && (krem & 15)) {
-      if (!A_MN) zero_tail_kc(dA, krem, tid);
-      if (B_KC) zero_tail_kc(dB, krem, tid);
-      __syncthreads();
-    }
+  auto issue_all = [&](int kt, uint8_t* dA, uint8_t* dB) {
+#pragma unroll
+    for (int j = 0; j < LOADS_PER_STEP; ++j) issue_one(j, kt, dA, dB);
+  };
+  // The partial last step's stage, once landed: clear the KC bytes >= K.
+  auto zero_tail = [&](uint8_t* dA, uint8_t* dB) {
+    if (!A_MN) zero_tail_kc(dA, krem, tid);
+    if (B_KC) zero_tail_kc(dB, krem, tid);
+    __syncthreads();
   };
 
   v4f acc[MI][NI];
@@ -295,18 +276,90 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
 
   const int wm = (wave / WAVES_N) * WTM;  // wave sub-tile
   const int wn = (wave % WAVES_N) * WTN;
+  constexpr int DSA = A_MN ? 4 : 2;  // LDS reads per A fragment
+  constexpr int DSB = B_KC ? 2 : 4;  // LDS reads per B fragment
 
-  if (KT > 0) issue(0, sA0, sB0);
-  for (int kt = 0; kt < KT; ++kt) {
+  v8i a[MI];      // A fragments of the step
+  v8i b, b_last;  // B fragment in use; the step's last B fragment
+
+  // One k-step. LOADS: issue the loads of step kt + 2 into this step's
+  // stage after the barrier. NEXT: step kt + 1 exists (barrier, then its A
+  // fragments and first B fragment are read into a[] and b).
+  auto step = [&](auto loads_tag, auto next_tag, int kt) {
+    constexpr bool LOADS = decltype(loads_tag)::value;
+    constexpr bool NEXT = decltype(next_tag)::value;
     const bool odd = kt & 1;
-    uint8_t* cA = odd ? sA1 : sA0;
+    uint8_t* cA = odd ? sA1 : sA0;  // this step's stage
     uint8_t* cB = odd ? sB1 : sB0;
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    uint8_t* nA = odd ? sA0 : sA1;  // the next step's stage
+    uint8_t* nB = odd ? sB0 : sB1;
+    // B column groups 0 .. NI - 3, the next group's fragment read ahead
+    static_for<0, NI - 2>([&](auto I) {
+      constexpr int ni = decltype(I)::value;
+      const v8i bn = read_frag<B_KC>(cB, wn + 16 * (ni + 1), lane);
+#pragma unroll
+      for (int mi = 0; mi < MI; ++mi) acc[mi][ni] = mfma<FA, FB>(b, a[mi], acc[mi][ni]);
+      b = bn;
+#pragma unroll
+      for (int mi = 0; mi < MI; ++mi) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        if (mi < DSB) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+    });
+    b_last = read_frag<B_KC>(cB, wn + 16 * (NI - 1), lane);
+    if (NEXT) {
+      // Every wave holds all B fragments of this step once its LDS reads
+      // have returned (the barrier waits for them), so this stage is free
+      // after the barrier; step kt + 1 has landed once every wave's loads
+      // have completed.
+      wait_vmcnt<0>();
+      __builtin_amdgcn_sched_barrier(0);
+      __syncthreads();
+      __builtin_amdgcn_sched_barrier(0);
+      if (!LOADS && kt + 1 == KT_full && (krem & 15)) zero_tail(nA, nB);
+    }
+    // B column groups NI - 2 and NI - 1, taken row block by row block: once
+    // both MFMAs of a[mi] have issued, a[mi] is refilled with the fragment
+    // of step kt + 1; the loads of step kt + 2 go out two per row block.
+    static_assert(LOADS_PER_STEP == 2 * MI, "two loads per row block");
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi) {
+      acc[mi][NI - 2] = mfma<FA, FB>(b, a[mi], acc[mi][NI - 2]);
+      acc[mi][NI - 1] = mfma<FA, FB>(b_last, a[mi], acc[mi][NI - 1]);
+      if (LOADS) {
+        issue_one(2 * mi, kt + 2, cA, cB);
+        issue_one(2 * mi + 1, kt + 2, cA, cB);
+      }
+      if (NEXT) a[mi] = read_frag<!A_MN>(nA, wm + 16 * mi, lane);
+    }
+    if (NEXT) b = read_frag<B_KC>(nB, wn, lane);
+    static_for<0, MI>([&](auto I) {
+      constexpr int i = decltype(I)::value;
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      if (NEXT) __builtin_amdgcn_sched_group_barrier(0x100, i + 1 < MI ? DSA : DSA + DSB, 0);
+    });
+  };
+
+  if (KT > 0) {
+    issue_all(0, sA0, sB0);
+    if (KT > 1) {
+      issue_all(1, sA1, sB1);
+      wait_vmcnt<LOADS_PER_STEP>();
+    } else {
+      wait_vmcnt<0>();
+    }
     __syncthreads();
-    fix_tail(kt, cA, cB);
-    if (kt + 1 < KT) issue(kt + 1, odd ? sA0 : sA1, odd ? sB0 : sB1);
-    mma_step<A_MN, B_KC, FA, FB>(acc, cA, cB, wm, wn, lane);
+    if (KT_full == 0 && (krem & 15)) zero_tail(sA0, sB0);
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi) a[mi] = read_frag<!A_MN>(sA0, wm + 16 * mi, lane);
+    b = read_frag<B_KC>(sB0, wn, lane);
   }
+  using T_ = std::true_type;
+  using F_ = std::false_type;
+  int kt = 0;
+  for (; kt + 2 < KT; ++kt) step(T_{}, T_{}, kt);
+  if (kt + 1 < KT) step(F_{}, T_{}, kt++);
+  if (kt < KT) step(F_{}, F_{}, kt);
 
   // ---- epilogue: lane holds C[m][n..n+3] for each (mi, ni)
   float lmax = 0.f;
@@ -341,7 +394,7 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
     }
   });
   // amax of |acc| over the valid elements (fmaxf ignores NaN): wave
-  // butterfly, then across the 4 waves, then one atomic max per workgroup
+  // butterfly, then across the waves, then one atomic max per workgroup
   // on the fp32 bits (non-negative floats order like their bits).
   for (int off = 32; off > 0; off >>= 1) lmax = fmaxf(lmax, __shfl_xor(lmax, off, 64));
   if (lane == 0) red[wave] = lmax;
