@@ -10,12 +10,19 @@ stream) and the CPU oracle timed on a bounded sample of the same workload.
 
   python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
   python bench.py --sweep      # also time every benchmark configuration
+  python bench.py --copy-calibration   # also run a 256 MiB device copy (PMC scale)
+
+`roofline.traffic` (HBM bytes per launch of the fused GEMM) comes from the
+rocprofv3 FETCH_SIZE / WRITE_SIZE summary committed under profiles/, and is
+reported only while the GEMM sources still hash to the value recorded there.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -26,6 +33,9 @@ METRIC = "scaled-FP8 GEMM TFLOP/s incl. rescale+cast; % of MI355X FP8 MFMA peak"
 PEAK_FP8_TFLOPS = 5000.0      # MI355X dense FP8 MFMA, 256 CU x 2.4 GHz x 8192 FLOP/clk
 PEAK_HBM_GBS = 8000.0
 FMT_NAME = {0: "e4m3", 1: "e5m2", 2: "f16"}
+GEMM_SOURCES = ("paper_2407_17353_amd/csrc/gemm_kernel.h", "paper_2407_17353_amd/csrc/gemm_nn.hip",
+                "paper_2407_17353_amd/csrc/codec.h", "paper_2407_17353_amd/csrc/kernels.h")
+TRAFFIC_SUMMARY = "profiles/gemm_8192cube_e4m3_hbm_traffic.md"
 
 
 def parse():
@@ -37,7 +47,43 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="target CPU time of the oracle sample")
     p.add_argument("--sweep", action="store_true", help="also time every configuration")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="also run a plain 256 MiB device-to-device copy 5 times (the known-size "
+                        "kernel that scales rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     return p.parse_args()
+
+
+def gemm_source_hash():
+    h = hashlib.sha256()
+    for rel in GEMM_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per launch of the 8192^3 GEMM from the committed rocprofv3
+    summary, or None when it is missing or was taken on other GEMM sources."""
+    path = os.path.join(ROOT, TRAFFIC_SUMMARY)
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m_hash = re.search(r"gemm source hash: ([0-9a-f]{16})", text)
+    m_bytes = re.search(r"HBM bytes per launch: ([0-9]+)", text)
+    if not m_hash or not m_bytes or m_hash.group(1) != gemm_source_hash():
+        return None
+    return int(m_bytes.group(1))
+
+
+def copy_calibration(dev, nbytes=256 << 20, reps=5):
+    """A plain device copy of known size, for scaling the PMC byte counters."""
+    import torch
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
 
 
 def time_case(case, steps, warmup, dev, ws=None):
@@ -59,22 +105,26 @@ def time_case(case, steps, warmup, dev, ws=None):
     for _ in range(warmup):
         sc.scalify_matmul(a, b, out, rescale=case.mode, ws=ws)
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
-    t0 = torch.cuda.Event(enable_timing=True)
-    t1 = torch.cuda.Event(enable_timing=True)
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
-    t0.record(stream)
+    marks[0].record(stream)
     for k in range(steps):
         sc.scalify_matmul(a, b, out, rescale=case.mode, ws=ws, events=evs[k])
-    t1.record(stream)
+        marks[k + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    total_ms = t0.elapsed_time(t1)
+    total_ms = marks[0].elapsed_time(marks[-1])
+    calls = sorted(marks[k].elapsed_time(marks[k + 1]) for k in range(steps))
     gemm_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / steps
     cast_ms = sum(e[1].elapsed_time(e[2]) for e in evs) / steps
+
+    def pct(q):
+        return calls[min(steps - 1, int(q * (steps - 1) + 0.5))]
     del A, B, a, b, out
     return {"ms_per_step": total_ms / steps, "wall_ms_per_step": wall * 1e3 / steps,
-            "gemm_ms": gemm_ms, "cast_ms": cast_ms}, ws
+            "gemm_ms": gemm_ms, "cast_ms": cast_ms,
+            "call_ms_p10": pct(0.1), "call_ms_p50": pct(0.5), "call_ms_p90": pct(0.9)}, ws
 
 
 def cpu_baseline(case, target_s):
@@ -121,6 +171,8 @@ def main():
         hip_build.build()
     sc.load_library()
     dev = "cuda:0"
+    if args.copy_calibration:
+        copy_calibration(dev)
     case = wl.config_4(8192, wl.E4M3)[0]
     res, ws = time_case(case, args.steps, args.warmup, dev)
     flops = case.flops
@@ -145,11 +197,14 @@ def main():
                    "out_fmt": "e4m3", "layout": "A [M][K], B [K][N]",
                    "scales_log2": [case.a_scale_log2, case.b_scale_log2]},
         "pct_of_peak": round(100.0 * value / PEAK_FP8_TFLOPS, 2),
+        "call_us_p10_p50_p90": [round(res[k] * 1e3, 1)
+                                for k in ("call_ms_p10", "call_ms_p50", "call_ms_p90")],
         "gemm_kernel_us": round(res["gemm_ms"] * 1e3, 2),
         "epilogue_cast_us": round(res["cast_ms"] * 1e3, 2),
         "roofline": {"bound": "mfma", "achieved": round(gemm_tflops, 2),
                      "peak": PEAK_FP8_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(gemm_tflops / PEAK_FP8_TFLOPS, 4), "traffic": None},
+                     "frac": round(gemm_tflops / PEAK_FP8_TFLOPS, 4),
+                     "traffic": measured_traffic()},
     }
     if args.sweep:
         sweep = []

@@ -14,6 +14,8 @@
 //     buffer_load_dwordx4 ... lds (16 B per lane, no VGPR staging) into two
 //     64 KiB stages. Buffer loads are range-checked: rows past the matrix,
 //     and K past its end, read as zeros without touching memory.
+//   * B fragments are read from LDS two column groups (8 MFMAs of the wave)
+//     ahead of their use.
 //   * Software pipeline with one barrier per step, placed before the last
 //     quarter of the step's MFMAs: by then every wave holds the B fragments
 //     it still needs, so after the barrier the step's stage is free and
@@ -279,8 +281,8 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
   constexpr int DSA = A_MN ? 4 : 2;  // LDS reads per A fragment
   constexpr int DSB = B_KC ? 2 : 4;  // LDS reads per B fragment
 
-  v8i a[MI];      // A fragments of the step
-  v8i b, b_last;  // B fragment in use; the step's last B fragment
+  v8i a[MI];   // A fragments of the step
+  v8i bq[3];   // B fragments: in use and up to two groups ahead
 
   // One k-step. LOADS: issue the loads of step kt + 2 into this step's
   // stage after the barrier. NEXT: step kt + 1 exists (barrier, then its A
@@ -293,20 +295,18 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
     uint8_t* cB = odd ? sB1 : sB0;
     uint8_t* nA = odd ? sA0 : sA1;  // the next step's stage
     uint8_t* nB = odd ? sB0 : sB1;
-    // B column groups 0 .. NI - 3, the next group's fragment read ahead
+    // B column groups 0 .. NI - 3, fragments read two groups ahead
     static_for<0, NI - 2>([&](auto I) {
       constexpr int ni = decltype(I)::value;
-      const v8i bn = read_frag<B_KC>(cB, wn + 16 * (ni + 1), lane);
+      bq[(ni + 2) % 3] = read_frag<B_KC>(cB, wn + 16 * (ni + 2), lane);
 #pragma unroll
-      for (int mi = 0; mi < MI; ++mi) acc[mi][ni] = mfma<FA, FB>(b, a[mi], acc[mi][ni]);
-      b = bn;
+      for (int mi = 0; mi < MI; ++mi) acc[mi][ni] = mfma<FA, FB>(bq[ni % 3], a[mi], acc[mi][ni]);
 #pragma unroll
       for (int mi = 0; mi < MI; ++mi) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         if (mi < DSB) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       }
     });
-    b_last = read_frag<B_KC>(cB, wn + 16 * (NI - 1), lane);
     if (NEXT) {
       // Every wave holds all B fragments of this step once its LDS reads
       // have returned (the barrier waits for them), so this stage is free
@@ -324,19 +324,22 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
     static_assert(LOADS_PER_STEP == 2 * MI, "two loads per row block");
 #pragma unroll
     for (int mi = 0; mi < MI; ++mi) {
-      acc[mi][NI - 2] = mfma<FA, FB>(b, a[mi], acc[mi][NI - 2]);
-      acc[mi][NI - 1] = mfma<FA, FB>(b_last, a[mi], acc[mi][NI - 1]);
+      acc[mi][NI - 2] = mfma<FA, FB>(bq[(NI - 2) % 3], a[mi], acc[mi][NI - 2]);
+      acc[mi][NI - 1] = mfma<FA, FB>(bq[(NI - 1) % 3], a[mi], acc[mi][NI - 1]);
       if (LOADS) {
         issue_one(2 * mi, kt + 2, cA, cB);
         issue_one(2 * mi + 1, kt + 2, cA, cB);
       }
       if (NEXT) a[mi] = read_frag<!A_MN>(nA, wm + 16 * mi, lane);
     }
-    if (NEXT) b = read_frag<B_KC>(nB, wn, lane);
+    if (NEXT) {
+      bq[0] = read_frag<B_KC>(nB, wn, lane);
+      bq[1] = read_frag<B_KC>(nB, wn + 16, lane);
+    }
     static_for<0, MI>([&](auto I) {
       constexpr int i = decltype(I)::value;
       __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-      if (NEXT) __builtin_amdgcn_sched_group_barrier(0x100, i + 1 < MI ? DSA : DSA + DSB, 0);
+      if (NEXT) __builtin_amdgcn_sched_group_barrier(0x100, i + 1 < MI ? DSA : DSA + 2 * DSB, 0);
     });
   };
 
@@ -352,7 +355,8 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
     if (KT_full == 0 && (krem & 15)) zero_tail(sA0, sB0);
 #pragma unroll
     for (int mi = 0; mi < MI; ++mi) a[mi] = read_frag<!A_MN>(sA0, wm + 16 * mi, lane);
-    b = read_frag<B_KC>(sB0, wn, lane);
+    bq[0] = read_frag<B_KC>(sB0, wn, lane);
+    bq[1] = read_frag<B_KC>(sB0, wn + 16, lane);
   }
   using T_ = std::true_type;
   using F_ = std::false_type;
