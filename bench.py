@@ -41,8 +41,10 @@ TRAFFIC_SUMMARY = "profiles/gemm_8192cube_e4m3_hbm_traffic.md"
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=50)
-    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--steps", type=int, default=100)
+    # The GEMM settles at its steady clock after some 40 back-to-back calls
+    # (the first ones run up to 15 % slower): warm up for ~50 ms.
+    p.add_argument("--warmup", type=int, default=100)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="target CPU time of the oracle sample")
@@ -210,7 +212,7 @@ def main():
         sweep = []
         for cfg, cases in wl.all_configs().items():
             for c in cases:
-                r, ws = time_case(c, max(5, args.steps // 5), 2, dev, ws)
+                r, ws = time_case(c, max(5, args.steps // 5), 20, dev, ws)
                 tf = c.flops / (r["ms_per_step"] * 1e-3) / 1e12
                 row = {"config": cfg, "name": c.name, "M": c.M, "N": c.N, "K": c.K,
                        "us": round(r["ms_per_step"] * 1e3, 1), "tflops": round(tf, 1),
