@@ -25,7 +25,7 @@ import subprocess
 import numpy as np
 
 E4M3, E5M2, F16, F32 = 0, 1, 2, 3
-RESCALE_NONE, RESCALE_AMAX = 0, 1
+RESCALE_NONE, RESCALE_AMAX, RESCALE_DELAYED = 0, 1, 2
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "scalify_oracle.c")
@@ -70,6 +70,9 @@ def _load():
     lib.or_matmul_epilogue.argtypes = [vp, c_i64, c_f32, c_f32, c_i64, c_int, c_i32, c_int,
                                        c_int, vp, ctypes.POINTER(c_i32), ctypes.POINTER(c_f32)]
     lib.or_matmul_epilogue.restype = c_int
+    lib.or_matmul_epilogue_delayed.argtypes = [vp, c_i64, c_f32, c_f32, c_i64, c_f32, c_i32, c_int,
+                                                c_int, vp, vp, vp]
+    lib.or_matmul_epilogue_delayed.restype = c_int
     lib.or_rescale.argtypes = [c_int, vp, c_i64, c_f32, c_int, c_i32, c_int, c_int, vp,
                                ctypes.POINTER(c_i32), ctypes.POINTER(c_f32)]
     lib.or_rescale.restype = c_int
@@ -182,6 +185,25 @@ def matmul_epilogue(acc: np.ndarray, s_a: float, s_b: float, K: int, mode: int =
     rc = lib.or_matmul_epilogue(_ptr(acc), acc.size, s_a, s_b, int(K), mode, target_log2,
                                 int(bool(saturate)), out_fmt, _ptr(out),
                                 ctypes.byref(e_out), ctypes.byref(amax))
+    if rc != 0:
+        raise ValueError("input scales must be finite powers of two")
+    return out, int(e_out.value), float(amax.value)
+
+
+def matmul_epilogue_delayed(acc: np.ndarray, s_a: float, s_b: float, K: int, amax_in: float,
+                            target_log2: int = 0, saturate: bool = True, out_fmt: int = E4M3):
+    """Delayed rescaling (Section 3.3): scale propagation and cast as in
+    matmul_epilogue, with the rescale exponent taken from amax_in, the
+    statistic recorded by an earlier call. Returns (codes, e_out, amax) where
+    amax is this call's statistic (max |acc * 2^-e_c|), for the next call."""
+    lib = _load()
+    acc = np.ascontiguousarray(acc, dtype=np.float32)
+    out = np.empty(acc.shape, dtype=_code_dtype(out_fmt))
+    e_out = ctypes.c_int32(0)
+    amax = ctypes.c_float(0)
+    rc = lib.or_matmul_epilogue_delayed(_ptr(acc), acc.size, s_a, s_b, int(K), float(amax_in),
+                                        target_log2, int(bool(saturate)), out_fmt, _ptr(out),
+                                        ctypes.byref(e_out), ctypes.byref(amax))
     if rc != 0:
         raise ValueError("input scales must be finite powers of two")
     return out, int(e_out.value), float(amax.value)

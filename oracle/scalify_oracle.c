@@ -32,7 +32,7 @@
 #include <math.h>
 
 enum { OR_E4M3 = 0, OR_E5M2 = 1, OR_F16 = 2, OR_F32 = 3 };
-enum { OR_RESCALE_NONE = 0, OR_RESCALE_AMAX = 1 };
+enum { OR_RESCALE_NONE = 0, OR_RESCALE_AMAX = 1, OR_RESCALE_DELAYED = 2 };
 
 /* ------------------------------------------------------------------------ */
 /* Number formats: closed-form decode (OCP FP8 E4M3 / E5M2, IEEE binary16).  */
@@ -350,15 +350,20 @@ int32_t or_rescale_exponent(float amax, int any, int32_t t)
 
 /* Shared tail of the matmul epilogue and of rescale: given fp32 values v
  * whose true value is v * 2^e_in, choose the output scale exponent and cast.
- *   mode NONE: e_want = e_in;  mode AMAX: e_want = e_in + e_r.
+ *   mode NONE: e_want = e_in;  mode AMAX: e_want = e_in + e_r(amax of v);
+ *   mode DELAYED: e_want = e_in + e_r(stat_in), stat_in from an earlier call.
  *   e_out = clamp(e_want) to the E8M0 range;  data' = ldexp(v, e_in - e_out).
  * One power-of-two shift of the exact fp32 value, then one rounding. */
 static int32_t finish(const float* v, int64_t n, int32_t e_in, int mode, int32_t t,
-                      int sat, int out_fmt, void* out, float* amax_out)
+                      int sat, int out_fmt, void* out, float* amax_out, float stat_in)
 {
     int any;
     float amax = or_amax(v, n, &any);
-    int32_t e_r = (mode == OR_RESCALE_AMAX) ? or_rescale_exponent(amax, any, t) : 0;
+    int32_t e_r = 0;
+    if (mode == OR_RESCALE_AMAX) e_r = or_rescale_exponent(amax, any, t);
+    /* DELAYED: the statistic recorded by an earlier call; a NaN one counts
+     * as "nothing measured", like an all-NaN tensor in AMAX mode. */
+    if (mode == OR_RESCALE_DELAYED) e_r = or_rescale_exponent(stat_in, !isnan(stat_in), t);
     int32_t e_out = clamp_e8m0(e_in + e_r);
     int32_t shift = e_in - e_out;
     int64_t i;
@@ -381,9 +386,9 @@ static int32_t finish(const float* v, int64_t n, int32_t e_in, int mode, int32_t
  *   value of data = data * 2^(e_a + e_b + e_c).
  * Returns 0 on success, -1 on a non-power-of-two input scale.
  * Outputs: codes, *e_out (output scale = 2^e_out), *amax (of acc*2^-e_c). */
-int or_matmul_epilogue(const float* acc, int64_t n, float s_a, float s_b, int64_t K,
-                       int mode, int32_t t, int sat, int out_fmt,
-                       void* out, int32_t* e_out, float* amax)
+static int matmul_epilogue_impl(const float* acc, int64_t n, float s_a, float s_b, int64_t K,
+                                int mode, int32_t t, int sat, int out_fmt,
+                                void* out, int32_t* e_out, float* amax, float stat_in)
 {
     int ok_a = 1, ok_b = 1;
     int32_t e_a = or_scale_exponent(s_a, &ok_a);
@@ -396,9 +401,29 @@ int or_matmul_epilogue(const float* acc, int64_t n, float s_a, float s_b, int64_
     for (i = 0; i < n; ++i) data[i] = ldexpf(acc[i], -e_c);
     /* The propagated data carries 2^(e_a+e_b+e_c). finish() shifts acc-based
      * data by e_in - e_out, which equals -(e_r) plus any clamp correction. */
-    *e_out = finish(data, n, e_a + e_b + e_c, mode, t, sat, out_fmt, out, amax);
+    *e_out = finish(data, n, e_a + e_b + e_c, mode, t, sat, out_fmt, out, amax, stat_in);
     free(data);
     return 0;
+}
+
+int or_matmul_epilogue(const float* acc, int64_t n, float s_a, float s_b, int64_t K,
+                       int mode, int32_t t, int sat, int out_fmt,
+                       void* out, int32_t* e_out, float* amax)
+{
+    if (mode != OR_RESCALE_NONE && mode != OR_RESCALE_AMAX) return -2;
+    return matmul_epilogue_impl(acc, n, s_a, s_b, K, mode, t, sat, out_fmt, out, e_out, amax, 0.0f);
+}
+
+/* Delayed rescaling (Section 3.3): as the epilogue above, with the rescale
+ * exponent taken from amax_in, the statistic an earlier call recorded
+ * (e_r = floor(log2 amax_in) - t; 0 when amax_in is 0, +Inf or NaN). The
+ * amax this call measures is returned in *amax for the next call. */
+int or_matmul_epilogue_delayed(const float* acc, int64_t n, float s_a, float s_b, int64_t K,
+                               float amax_in, int32_t t, int sat, int out_fmt,
+                               void* out, int32_t* e_out, float* amax)
+{
+    return matmul_epilogue_impl(acc, n, s_a, s_b, K, OR_RESCALE_DELAYED, t, sat, out_fmt,
+                                out, e_out, amax, amax_in);
 }
 
 /* Full scaled matmul: accumulate then epilogue. acc_out may be NULL. */
@@ -443,7 +468,7 @@ int or_rescale(int in_fmt, const void* in, int64_t n, float s_in,
     if (!ok) return -1;
     v = (float*)malloc(sizeof(float) * (size_t)(n > 0 ? n : 1));
     decode_to_f32(in_fmt, in, n, v);
-    *e_out = finish(v, n, e_in, mode, t, sat, out_fmt, out, amax);
+    *e_out = finish(v, n, e_in, mode, t, sat, out_fmt, out, amax, 0.0f);
     free(v);
     return 0;
 }

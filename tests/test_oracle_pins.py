@@ -434,3 +434,60 @@ def test_nan_sign_is_kept_through_decode_and_cast():
     assert list(orc.cast_data(codes, orc.E4M3, orc.F16)) == [0x7E00, 0xFE00]
     ref = torch.from_numpy(np.array([np.nan, -np.nan], np.float32)).to(torch.float8_e4m3fn)
     assert list(ref.view(torch.uint8).numpy()) == [0x7F, 0xFF]
+
+
+# ------------------------------------------------------------------ delayed rescale
+
+def test_delayed_hand_examples():
+    """Delayed rescaling (Section 3.3): hand-derived cases, tests/golden/delayed_examples.json."""
+    with open(os.path.join(GOLDEN, "delayed_examples.json")) as f:
+        cases = json.load(f)["cases"]
+    fmt_of = {"e4m3": orc.E4M3, "e5m2": orc.E5M2, "f16": orc.F16}
+    for c in cases:
+        acc = np.array(c["acc"], dtype=np.float32)
+        codes, e_out, amax = orc.matmul_epilogue_delayed(
+            acc, 2.0 ** c["a_scale_log2"], 2.0 ** c["b_scale_log2"], c["K"], c["amax_in"],
+            saturate=c["saturate"], out_fmt=fmt_of[c["out_fmt"]])
+        assert codes.tolist() == c["out_codes"], c["name"]
+        assert e_out == c["out_scale_log2"], c["name"]
+        assert amax == c["amax"], c["name"]
+
+
+@pytest.mark.parametrize("out_fmt", [orc.E4M3, orc.E5M2, orc.F16])
+@pytest.mark.parametrize("target", [0, 3])
+def test_delayed_with_the_current_statistic_is_the_dynamic_rescale(out_fmt, target):
+    """Fed this call's own amax, the delayed rescale is the dynamic one."""
+    rng = np.random.default_rng(7 + out_fmt + 10 * target)
+    acc = (rng.standard_normal((37, 29)) * 2.0 ** rng.integers(-6, 9, (37, 29))).astype(np.float32)
+    K = 300
+    dyn = orc.matmul_epilogue(acc, 2.0 ** -3, 2.0 ** 2, K, orc.RESCALE_AMAX, target, True, out_fmt)
+    dl = orc.matmul_epilogue_delayed(acc, 2.0 ** -3, 2.0 ** 2, K, dyn[2], target, True, out_fmt)
+    assert np.array_equal(dyn[0], dl[0]) and dyn[1] == dl[1] and dyn[2] == dl[2]
+
+
+@pytest.mark.parametrize("stat", [0.0, float("inf"), float("nan")])
+def test_delayed_without_a_statistic_is_the_static_rule(stat):
+    """amax_in of 0, +Inf or NaN measures nothing: no rebalance (NONE mode)."""
+    rng = np.random.default_rng(11)
+    acc = (rng.standard_normal(500) * 40).astype(np.float32)
+    ref = orc.matmul_epilogue(acc, 1.0, 0.5, 64, orc.RESCALE_NONE, 0, True, orc.E4M3)
+    dl = orc.matmul_epilogue_delayed(acc, 1.0, 0.5, 64, stat, 0, True, orc.E4M3)
+    assert np.array_equal(ref[0], dl[0]) and ref[1] == dl[1] and ref[2] == dl[2]
+
+
+def test_delayed_stale_statistic_saturates_exactly_past_the_rounding_boundary():
+    """A statistic 2^j too small scales the data up by 2^j, so the largest
+    magnitudes leave the E4M3 range. The max code 0x7E (448) must then be
+    exactly the elements with |data'| >= 432: from 432 (the tie between 416
+    and 448, which goes to the even code 448) up to 464 they round to 448,
+    above 464 they overflow and saturate to 448."""
+    v = np.arange(1, 2001, dtype=np.float32) / 8.0          # 0.125 .. 250, exact
+    acc = np.concatenate([v, -v])
+    stat = 0.25                                              # far below the amax of 250
+    codes, e_out, _ = orc.matmul_epilogue_delayed(acc, 1.0, 1.0, 1, stat, 0, True, orc.E4M3)
+    e_r = -2
+    scaled = np.abs(acc.astype(np.float64)) * 2.0 ** (-e_r)   # exact: 0.5 .. 1000
+    sat = (codes & 0x7F) == 0x7E
+    assert e_out == e_r
+    assert 0 < sat.sum() < sat.size
+    assert np.array_equal(sat, scaled >= 432.0)              # 432 is the midpoint of 416 and 448
