@@ -63,8 +63,9 @@ typedef enum {
 } scalify_dtype;
 
 typedef enum {
-    SCALIFY_RESCALE_NONE = 0, /* static propagation rule only */
-    SCALIFY_RESCALE_AMAX = 1  /* dynamic power-of-two rescale from the amax */
+    SCALIFY_RESCALE_NONE = 0,   /* static propagation rule only */
+    SCALIFY_RESCALE_AMAX = 1,   /* dynamic power-of-two rescale from this call's amax */
+    SCALIFY_RESCALE_DELAYED = 2 /* delayed rescale: from the amax an earlier call recorded */
 } scalify_rescale_mode;
 
 /* A ScaledArray (Section 2, Section 3.1): value = decode(data) * (*scale).
@@ -92,8 +93,12 @@ typedef struct {
     float* acc_out;      /* optional device [M][N] fp32: the raw accumulator sum_k a_ik b_kj */
     float* amax_out;     /* optional device fp32: amax of acc * 2^-e_c over non-NaN elements */
     void** events;       /* optional host array of 3 hipEvent_t recorded on the stream: before
-                            the GEMM kernel, after it, and after the epilogue cast (timing of
-                            the fused GEMM without host synchronisation); NULL = none */
+                            the GEMM kernel, after it, and after the epilogue cast (DELAYED:
+                            after the amax write-back) -- timing of the fused GEMM without
+                            host synchronisation; NULL = none */
+    const float* amax_in; /* DELAYED only (required there): device fp32 statistic recorded by
+                            an earlier call (its amax_out); may be the same memory as
+                            amax_out, it is read before this call writes its own */
 } scalify_matmul_opts;
 
 /* Exponent e_c of the matmul scale rule (Section 3.2, Algorithm 3): the
@@ -102,18 +107,25 @@ typedef struct {
 int32_t scalify_matmul_scale_log2(int64_t K);
 
 /* Bytes of device workspace scalify_matmul needs for an M x N output with
- * the given output type and rescale mode: a 256-byte header plus the
- * pre-cast intermediate (M rows of N rounded up to 16 elements; 2 bytes per
- * element for FP8 outputs, 4 for FP16). Returns 0 for invalid arguments. */
+ * the given output type and rescale mode: a 256-byte header plus, for NONE
+ * and AMAX, the pre-cast intermediate (M rows of N rounded up to 16
+ * elements; 2 bytes per element for FP8 outputs, 4 for FP16). DELAYED needs
+ * the header only. Returns 0 for invalid arguments. */
 size_t scalify_matmul_workspace_size(int64_t M, int64_t N, int32_t out_dtype, int32_t rescale);
 
 /* Scaled matmul on ScaledArray operands (Section 3.2, Algorithm 3; FP8
  * matmul with mixed input formats and higher-precision accumulation,
- * Appendix A), with the dynamic rescale (Section 3.3) fused:
+ * Appendix A), with the dynamic or delayed rescale (Section 3.3) fused:
  *   acc   = sum_k dec(a)[i,k] * dec(b)[k,j]        fp32 accumulation (MFMA)
  *   e_c   = scalify_matmul_scale_log2(K)
  *   AMAX: e_r = floor(log2 amax(acc * 2^-e_c)) - target_log2
  *         (0 when that amax is 0 or +Inf or every element is NaN)
+ *   DELAYED: e_r = floor(log2 |*opts.amax_in|) - target_log2, the statistic
+ *         of an earlier call (0 when it is 0, Inf or NaN); this call's amax
+ *         (of acc * 2^-e_c) goes to opts.amax_out for the next call. Values
+ *         the stale scale pushes past the format's range saturate (or
+ *         overflow when saturate = 0). The GEMM writes the codes directly:
+ *         no intermediate, no second pass over the output.
  *   NONE: e_r = 0
  *   e_out = clamp(e_a + e_b + e_c + e_r, -127, 127)        (E8M0 range)
  *   out.data  = RNE(acc * 2^(e_a + e_b - e_out)) in out.dtype (saturating

@@ -16,7 +16,7 @@ from typing import Optional
 import torch
 
 E4M3, E5M2, F16, F32 = 0, 1, 2, 3
-RESCALE_NONE, RESCALE_AMAX = 0, 1
+RESCALE_NONE, RESCALE_AMAX, RESCALE_DELAYED = 0, 1, 2
 
 STATUS_NAMES = {0: "SCALIFY_OK", 1: "SCALIFY_ERR_NULL", 2: "SCALIFY_ERR_DTYPE",
                 3: "SCALIFY_ERR_SHAPE", 4: "SCALIFY_ERR_LAYOUT", 5: "SCALIFY_ERR_ALIGN",
@@ -45,7 +45,7 @@ class CMatmulOpts(ctypes.Structure):
     _fields_ = [("out_dtype", ctypes.c_int32), ("rescale", ctypes.c_int32),
                 ("target_log2", ctypes.c_int32), ("saturate", ctypes.c_int32),
                 ("acc_out", ctypes.c_void_p), ("amax_out", ctypes.c_void_p),
-                ("events", ctypes.c_void_p)]
+                ("events", ctypes.c_void_p), ("amax_in", ctypes.c_void_p)]
 
 
 EXPORTED = ("scalify_matmul_scale_log2", "scalify_matmul_workspace_size", "scalify_matmul",
@@ -152,12 +152,14 @@ def workspace(nbytes: int, device) -> torch.Tensor:
 
 def scalify_matmul(a: ScaledArray, b: ScaledArray, out: ScaledArray, *, rescale: int = RESCALE_AMAX,
                    target_log2: int = 0, saturate: bool = True, acc_out: torch.Tensor = None,
-                   amax_out: torch.Tensor = None, ws: torch.Tensor = None, stream=None,
-                   events=None) -> None:
-    """Scaled matmul (Section 3.2) with the fused dynamic rescale and cast
-    (Section 3.3); see scalify_matmul in include/scalify.h. `events`: an
-    optional sequence of 3 torch.cuda.Event(enable_timing=True) recorded
-    before the GEMM kernel, after it and after the epilogue cast."""
+                   amax_out: torch.Tensor = None, amax_in: torch.Tensor = None,
+                   ws: torch.Tensor = None, stream=None, events=None) -> None:
+    """Scaled matmul (Section 3.2) with the fused dynamic or delayed rescale
+    and cast (Section 3.3); see scalify_matmul in include/scalify.h.
+    `amax_in` (RESCALE_DELAYED): one-element fp32 device tensor holding the
+    statistic of an earlier call (its `amax_out`; may be the same tensor).
+    `events`: an optional sequence of 3 torch.cuda.Event(enable_timing=True)
+    recorded before the GEMM kernel, after it and after the epilogue."""
     lib = load_library()
     M, _ = a.shape
     _, N = b.shape
@@ -172,7 +174,8 @@ def scalify_matmul(a: ScaledArray, b: ScaledArray, out: ScaledArray, *, rescale:
     opts = CMatmulOpts(int(out.fmt), int(rescale), int(target_log2), int(bool(saturate)),
                        acc_out.data_ptr() if acc_out is not None else None,
                        amax_out.data_ptr() if amax_out is not None else None,
-                       ctypes.cast(ev_arr, ctypes.c_void_p) if ev_arr is not None else None)
+                       ctypes.cast(ev_arr, ctypes.c_void_p) if ev_arr is not None else None,
+                       amax_in.data_ptr() if amax_in is not None else None)
     ca, cb, co = a.c_struct(), b.c_struct(), out.c_struct()
     st = lib.scalify_matmul(ctypes.byref(ca), ctypes.byref(cb), ctypes.byref(co), ctypes.byref(opts),
                             ws.data_ptr(), ws.numel(), _stream_handle(stream))

@@ -31,6 +31,40 @@ hipError_t launch_prologue(uint32_t* hdr, const float* s0, const float* s1, hipS
   return hipGetLastError();
 }
 
+// Delayed rescale (Section 3.3): the rebalance uses the statistic an earlier
+// call recorded, so the output scale is known before the GEMM runs.
+__global__ void prologue_delayed_kernel(uint32_t* hdr, const float* s0, const float* s1,
+                                        const float* amax_in, int e_c, int target,
+                                        float* out_scale) {
+  if (threadIdx.x == 0) {
+    const int e_ab = pow2_exponent(s0) + pow2_exponent(s1);
+    const uint32_t stat = __float_as_uint(*amax_in) & 0x7FFFFFFFu;  // |statistic|
+    const int e_r = rescale_exponent(stat, target);  // 0 for 0, Inf, NaN
+    const int e_out = clamp_e8m0(e_ab + e_c + e_r);
+    hdr[0] = 0u;
+    hdr[1] = (uint32_t)e_ab;
+    hdr[2] = (uint32_t)(e_out - e_ab);
+    *out_scale = pow2_float(e_out);
+  }
+}
+
+hipError_t launch_prologue_delayed(uint32_t* hdr, const float* s0, const float* s1,
+                                   const float* amax_in, int e_c, int target, float* out_scale,
+                                   hipStream_t s) {
+  hipLaunchKernelGGL(prologue_delayed_kernel, dim3(1), dim3(64), 0, s, hdr, s0, s1, amax_in, e_c,
+                     target, out_scale);
+  return hipGetLastError();
+}
+
+__global__ void finalize_amax_kernel(const uint32_t* hdr, int e_c, float* amax_out) {
+  if (threadIdx.x == 0) *amax_out = __uint_as_float(hdr[0]) * pow2_float(-e_c);
+}
+
+hipError_t launch_finalize_amax(const uint32_t* hdr, int e_c, float* amax_out, hipStream_t s) {
+  hipLaunchKernelGGL(finalize_amax_kernel, dim3(1), dim3(64), 0, s, hdr, e_c, amax_out);
+  return hipGetLastError();
+}
+
 // Load 16 consecutive elements of format F as raw codes / fp32 bits.
 template <int F>
 __device__ __forceinline__ void load16(const void* base, int64_t e, uint32_t (&c)[16]) {

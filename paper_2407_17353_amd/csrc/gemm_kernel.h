@@ -2,8 +2,10 @@
 // accumulation of the scaled matmul (Scalify, Section 3.2 / Algorithm 3;
 // mixed E4M3/E5M2 inputs and higher-precision accumulation, Appendix A),
 // with its epilogue fused: the amax statistic of the dynamic rescale
-// (Section 3.3) and a compact pre-cast intermediate for the cast kernel
-// that follows (the rescale exponent needs the amax of the whole output).
+// (Section 3.3) and either a compact pre-cast intermediate for the cast
+// kernel that follows (the dynamic rescale exponent needs the amax of the
+// whole output) or, for the delayed rescale, whose output scale is known
+// before the GEMM starts, the output codes themselves.
 //
 // Design (per workgroup of 512 threads = 8 wave64, two per SIMD):
 //   * 256 x 256 output tile, K consumed in 128-byte steps; each wave owns a
@@ -215,6 +217,45 @@ __device__ __forceinline__ void static_for(F&& f) {
   }
 }
 
+// Direct cast of 4 accumulator values (fp32 bits) times 2^-shift, for the
+// delayed rescale. Fast paths use the hardware conversions (callers check
+// that |shift| <= kFastShiftMax and that no value is NaN); the exact integer
+// casts are kept out of line.
+__device__ __forceinline__ v2i cast4_f16_hw(uint32_t u0, uint32_t u1, uint32_t u2, uint32_t u3,
+                                           float inv, bool sat) {
+  // x * 2^-shift (inv = 2^-shift) is exact in fp32 unless it leaves the
+  // fp32 normal range: above it the conversion overflows as the exact value
+  // would, below it the value rounds to zero in FP16 either way.
+  // v_cvt_f16_f32 then rounds to nearest even, keeping FP16 subnormals;
+  // overflow gives +-Inf, which saturation turns into +-max.
+  uint32_t h[4];
+  const uint32_t u[4] = {u0, u1, u2, u3};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const _Float16 f = (_Float16)(__uint_as_float(u[i]) * inv);
+    uint32_t b = (uint32_t)__builtin_bit_cast(uint16_t, f);
+    if (sat && (b & 0x7FFFu) == 0x7C00u) b -= 1u;  // +-Inf -> +-65504
+    h[i] = b;
+  }
+  return v2i{(int)(h[0] | (h[1] << 16)), (int)(h[2] | (h[3] << 16))};
+}
+
+__device__ __attribute__((noinline)) v2i cast4_slow_f16(uint32_t u0, uint32_t u1, uint32_t u2,
+                                                         uint32_t u3, int shift, bool sat) {
+  return v2i{(int)(cast_bits<kF16>(u0, shift, sat) | (cast_bits<kF16>(u1, shift, sat) << 16)),
+             (int)(cast_bits<kF16>(u2, shift, sat) | (cast_bits<kF16>(u3, shift, sat) << 16))};
+}
+
+__device__ __attribute__((noinline)) uint32_t cast4_slow_fp8(int fmt, uint32_t u0, uint32_t u1,
+                                                              uint32_t u2, uint32_t u3, int shift,
+                                                              bool sat) {
+  if (fmt == kE4M3)
+    return cast_bits<kE4M3>(u0, shift, sat) | (cast_bits<kE4M3>(u1, shift, sat) << 8) |
+           (cast_bits<kE4M3>(u2, shift, sat) << 16) | (cast_bits<kE4M3>(u3, shift, sat) << 24);
+  return cast_bits<kE5M2>(u0, shift, sat) | (cast_bits<kE5M2>(u1, shift, sat) << 8) |
+         (cast_bits<kE5M2>(u2, shift, sat) << 16) | (cast_bits<kE5M2>(u3, shift, sat) << 24);
+}
+
 template <bool A_MN, bool B_KC, int FA, int FB, int EPI>
 __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
   __shared__ __attribute__((aligned(1024))) uint8_t sA0[TILE_BYTES];
@@ -369,6 +410,12 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
   float lmax = 0.f;
   const int mb = m0 + wm + (lane & 15);
   const int nb = n0 + wn + 4 * (lane >> 4);
+  // EPI_DIRECT: data' = acc * 2^-shift, shift from the prologue
+  const int shift = EPI == EPI_DIRECT ? (int)__builtin_amdgcn_readfirstlane(p.hdr[2]) : 0;
+  const bool fast = shift >= -kFastShiftMax && shift <= kFastShiftMax;
+  const float hw_scale = fast ? pow2_float(shift) : 1.0f;
+  const float hw_inv = fast ? pow2_float(-shift) : 1.0f;
+  const bool sat = p.sat != 0;
   static_for<0, MI * NI>([&](auto I) {
     constexpr int mi = decltype(I)::value / NI, ni = decltype(I)::value % NI;
     const int m = mb + 16 * mi;
@@ -384,9 +431,49 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
         const uint32_t h2 = sticky16(__float_as_uint(v[2])), h3 = sticky16(__float_as_uint(v[3]));
         uint16_t* q = (uint16_t*)p.inter + (int64_t)m * p.ldw + n;
         *(v2i*)q = v2i{(int)(h0 | (h1 << 16)), (int)(h2 | (h3 << 16))};
-      } else {
+      } else if (EPI == EPI_INTER32) {
         float* q = (float*)p.inter + (int64_t)m * p.ldw + n;
         *(v4f*)q = v;
+      } else {
+        const uint32_t u0 = __float_as_uint(v[0]), u1 = __float_as_uint(v[1]);
+        const uint32_t u2 = __float_as_uint(v[2]), u3 = __float_as_uint(v[3]);
+        // Hardware conversions unless a lane of the wave holds a NaN or the
+        // shift is out of their range (then the exact integer cast, out of
+        // line: it is rare and large).
+        const bool nan = is_nan_bits(u0) || is_nan_bits(u1) || is_nan_bits(u2) || is_nan_bits(u3);
+        const bool hw = fast && !__any(nan);
+        if (p.out_fmt == kF16) {
+          v2i w;
+          if (hw) {
+            w = cast4_f16_hw(u0, u1, u2, u3, hw_inv, sat);
+          } else {
+            w = cast4_slow_f16(u0, u1, u2, u3, shift, sat);
+          }
+          uint16_t* q = (uint16_t*)p.out + (int64_t)m * p.ldc + n;
+          if (n + 3 < N) {
+            *(v2i*)q = w;
+          } else {
+            q[0] = (uint16_t)w.x;
+            if (n + 1 < N) q[1] = (uint16_t)((uint32_t)w.x >> 16);
+            if (n + 2 < N) q[2] = (uint16_t)w.y;
+          }
+        } else {
+          uint32_t w;
+          if (hw) {
+            w = p.out_fmt == kE4M3 ? cast4_fp8_hw<kE4M3>(u0, u1, u2, u3, hw_scale, sat)
+                                   : cast4_fp8_hw<kE5M2>(u0, u1, u2, u3, hw_scale, sat);
+          } else {
+            w = cast4_slow_fp8(p.out_fmt, u0, u1, u2, u3, shift, sat);
+          }
+          uint8_t* q = (uint8_t*)p.out + (int64_t)m * p.ldc + n;
+          if (n + 3 < N) {
+            *(uint32_t*)q = w;
+          } else {
+            q[0] = (uint8_t)w;
+            if (n + 1 < N) q[1] = (uint8_t)(w >> 8);
+            if (n + 2 < N) q[2] = (uint8_t)(w >> 16);
+          }
+        }
       }
       if (p.acc_out) {
         float* q = p.acc_out + (int64_t)m * N + n;

@@ -11,8 +11,11 @@ static hipError_t launch_fmt(const GemmParams& p, int epi, hipStream_t s) {
     case EPI_INTER16:
       hipLaunchKernelGGL((gemm_kernel<false, true, FA, FB, EPI_INTER16>), grid, block, 0, s, p);
       break;
-    default:
+    case EPI_INTER32:
       hipLaunchKernelGGL((gemm_kernel<false, true, FA, FB, EPI_INTER32>), grid, block, 0, s, p);
+      break;
+    default:
+      hipLaunchKernelGGL((gemm_kernel<false, true, FA, FB, EPI_DIRECT>), grid, block, 0, s, p);
       break;
   }
   return hipGetLastError();

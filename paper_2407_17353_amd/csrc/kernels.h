@@ -9,11 +9,14 @@ namespace scalify {
 //   [0] amax as fp32 bits (atomic max target; zeroed by the prologue)
 //   [1] exponent sum of the input scales (snapshot taken by the prologue, so
 //       that an output scale aliasing an input scale cannot race)
+//   [2] delayed rescale: the shift of the direct cast, data' = acc * 2^-shift
 constexpr size_t kHeaderBytes = 256;
 
-// Pre-cast intermediate written by the GEMM: 16-bit rounding-preserving
-// encoding (FP8 outputs) or the fp32 accumulator (FP16 outputs).
-enum Epi : int { EPI_INTER16 = 0, EPI_INTER32 = 1 };
+// What the GEMM writes: a pre-cast intermediate for the cast kernel that
+// follows (16-bit rounding-preserving encoding for FP8 outputs, the fp32
+// accumulator for FP16 outputs), or, when the output scale is known before
+// the GEMM runs (delayed rescale), the output codes themselves.
+enum Epi : int { EPI_INTER16 = 0, EPI_INTER32 = 1, EPI_DIRECT = 2 };
 
 struct GemmParams {
   const uint8_t* a;
@@ -28,6 +31,9 @@ struct GemmParams {
   void* inter;    // pre-cast intermediate [M][ldw] (EPI_INTER16: u16, EPI_INTER32: f32)
   int64_t ldw;
   float* acc_out;  // optional raw accumulator [M][N]
+  void* out;       // EPI_DIRECT: output codes [M][ldc] of format out_fmt
+  int64_t ldc;
+  int out_fmt;
 };
 
 hipError_t launch_gemm(const GemmParams& p, bool a_mn, bool b_kc, int fa, int fb, int epi,
@@ -35,6 +41,17 @@ hipError_t launch_gemm(const GemmParams& p, bool a_mn, bool b_kc, int fa, int fb
 
 // Prologue: hdr[0] = 0, hdr[1] = exponent(s0) + exponent(s1) (NULL = scale 1).
 hipError_t launch_prologue(uint32_t* hdr, const float* s0, const float* s1, hipStream_t s);
+
+// Prologue of the delayed rescale: as launch_prologue, plus the output scale
+// from the statistic *amax_in of an earlier call (e_r = floor(log2 amax_in)
+// - target, 0 when amax_in is 0, Inf or NaN): writes *out_scale = 2^e_out,
+// e_out = clamp(e_a + e_b + e_c + e_r), and hdr[2] = e_out - e_a - e_b.
+hipError_t launch_prologue_delayed(uint32_t* hdr, const float* s0, const float* s1,
+                                   const float* amax_in, int e_c, int target, float* out_scale,
+                                   hipStream_t s);
+
+// *amax_out = amax recorded in hdr[0] (max |acc|) times 2^-e_c.
+hipError_t launch_finalize_amax(const uint32_t* hdr, int e_c, float* amax_out, hipStream_t s);
 
 // Cast of the GEMM intermediate [M][ldw] to out [M][ldc]; computes the
 // rescale exponent from hdr and writes *out_scale (and *amax_out).

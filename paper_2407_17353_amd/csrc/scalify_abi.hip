@@ -35,7 +35,10 @@ scalify_status check_matrix(const scalify_scaled_array* x, int64_t ld_multiple) 
 }
 
 size_t matmul_ws(int64_t M, int64_t N, int32_t out_dtype, int32_t rescale) {
-  if (M < 0 || N < 0 || !is_out(out_dtype) || (rescale != 0 && rescale != 1)) return 0;
+  if (M < 0 || N < 0 || !is_out(out_dtype) || rescale < SCALIFY_RESCALE_NONE ||
+      rescale > SCALIFY_RESCALE_DELAYED)
+    return 0;
+  if (rescale == SCALIFY_RESCALE_DELAYED) return kHeaderBytes;  // codes written by the GEMM
   return kHeaderBytes + (size_t)M * (size_t)round_up(N, 16) * (out_dtype == SCALIFY_F16 ? 4u : 2u);
 }
 
@@ -100,8 +103,9 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
   if (!is_fp8(a->dtype) || !is_fp8(b->dtype) || !is_out(opts->out_dtype) ||
       out->dtype != opts->out_dtype)
     return SCALIFY_ERR_DTYPE;
-  if (opts->rescale != SCALIFY_RESCALE_NONE && opts->rescale != SCALIFY_RESCALE_AMAX)
+  if (opts->rescale < SCALIFY_RESCALE_NONE || opts->rescale > SCALIFY_RESCALE_DELAYED)
     return SCALIFY_ERR_VALUE;
+  if (opts->rescale == SCALIFY_RESCALE_DELAYED && !opts->amax_in) return SCALIFY_ERR_NULL;
   if (opts->target_log2 < -1000 || opts->target_log2 > 1000) return SCALIFY_ERR_VALUE;
   if (out->trans != 0) return SCALIFY_ERR_LAYOUT;
   const int64_t M = a->rows, K = a->cols, N = b->cols;
@@ -122,9 +126,18 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
   uint32_t* hdr = (uint32_t*)workspace;
   const int e_c = scalify_matmul_scale_log2(K);
   const bool amax_mode = opts->rescale == SCALIFY_RESCALE_AMAX;
-  const int epi = opts->out_dtype == SCALIFY_F16 ? EPI_INTER32 : EPI_INTER16;
+  const bool delayed = opts->rescale == SCALIFY_RESCALE_DELAYED;
+  const int epi = delayed ? EPI_DIRECT : (opts->out_dtype == SCALIFY_F16 ? EPI_INTER32 : EPI_INTER16);
 
-  if (launch_prologue(hdr, a->scale, b->scale, s) != hipSuccess) return SCALIFY_ERR_HIP;
+  if (delayed) {
+    // The output scale comes from the statistic of an earlier call, so the
+    // GEMM casts its accumulators straight to codes: no intermediate.
+    if (launch_prologue_delayed(hdr, a->scale, b->scale, opts->amax_in, e_c, opts->target_log2,
+                                out->scale, s) != hipSuccess)
+      return SCALIFY_ERR_HIP;
+  } else if (launch_prologue(hdr, a->scale, b->scale, s) != hipSuccess) {
+    return SCALIFY_ERR_HIP;
+  }
 
   GemmParams p = {};
   p.a = (const uint8_t*)a->data;
@@ -144,6 +157,9 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
   p.inter = (uint8_t*)workspace + kHeaderBytes;
   p.ldw = round_up(N, 16);
   p.acc_out = opts->acc_out;
+  p.out = out->data;
+  p.ldc = out->ld;
+  p.out_fmt = opts->out_dtype;
   hipEvent_t* ev = (hipEvent_t*)opts->events;
   if (ev && hipEventRecord(ev[0], s) != hipSuccess) return SCALIFY_ERR_HIP;
   if (M > 0 && N > 0) {
@@ -151,7 +167,11 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
       return SCALIFY_ERR_HIP;
   }
   if (ev && hipEventRecord(ev[1], s) != hipSuccess) return SCALIFY_ERR_HIP;
-  {
+  if (delayed) {
+    // The statistic this call records for the next one.
+    if (opts->amax_out && launch_finalize_amax(hdr, e_c, opts->amax_out, s) != hipSuccess)
+      return SCALIFY_ERR_HIP;
+  } else {
     // Second pass: global amax -> rescale exponent -> output scale, and the
     // cast of the intermediate (also for NONE mode, where e_r = 0).
     EpilogueParams q = {};

@@ -41,6 +41,10 @@ def test_workspace_sizes():
     assert sc.scalify_matmul_workspace_size(10, 10, sc.F16) == 256 + 10 * 16 * 4
     assert sc.scalify_matmul_workspace_size(10, 10, sc.F32) == 0      # not an output type
     assert sc.scalify_matmul_workspace_size(-1, 10, sc.E4M3) == 0
+    # the delayed rescale casts inside the GEMM: header only
+    assert sc.scalify_matmul_workspace_size(8192, 8192, sc.E4M3, sc.RESCALE_DELAYED) == 256
+    assert sc.scalify_matmul_workspace_size(10, 10, sc.F16, sc.RESCALE_DELAYED) == 256
+    assert sc.scalify_matmul_workspace_size(10, 10, sc.E4M3, 3) == 0
     assert sc.scalify_rescale_workspace_size(123) == 256
 
 
@@ -70,7 +74,7 @@ def call_matmul(a, b, out, opts=None, ws=FAKE + 8192, ws_bytes=1 << 40):
 
 @pytest.mark.parametrize("case,status", [
     ("null_scale_out", 1), ("bad_a_dtype", 2), ("f32_b", 2), ("out_dtype_mismatch", 2),
-    ("bad_mode", 7), ("bad_target", 7), ("out_trans", 4), ("k_mismatch", 3), ("n_mismatch", 3),
+    ("bad_mode", 7), ("delayed_without_statistic", 1), ("bad_target", 7), ("out_trans", 4), ("k_mismatch", 3), ("n_mismatch", 3),
     ("negative", 3), ("ld_small", 3), ("ld_unaligned", 5), ("ptr_unaligned", 5),
     ("ws_small", 6), ("ws_null", 6), ("ws_unaligned", 6), ("null_data", 1), ("too_big", 3),
 ])
@@ -86,7 +90,9 @@ def test_matmul_argument_errors(case, status):
     elif case == "out_dtype_mismatch":
         kw["opts"] = sc.CMatmulOpts(sc.E5M2, 1, 0, 1, None, None, None)
     elif case == "bad_mode":
-        kw["opts"] = sc.CMatmulOpts(sc.E4M3, 2, 0, 1, None, None, None)
+        kw["opts"] = sc.CMatmulOpts(sc.E4M3, 3, 0, 1, None, None, None)
+    elif case == "delayed_without_statistic":
+        kw["opts"] = sc.CMatmulOpts(sc.E4M3, sc.RESCALE_DELAYED, 0, 1, None, None, None, None)
     elif case == "bad_target":
         kw["opts"] = sc.CMatmulOpts(sc.E4M3, 1, 5000, 1, None, None, None)
     elif case == "out_trans":
