@@ -95,7 +95,8 @@ typedef struct {
     void** events;       /* optional host array of 3 hipEvent_t recorded on the stream: before
                             the GEMM kernel, after it, and after the epilogue cast (DELAYED:
                             after the amax write-back) -- timing of the fused GEMM without
-                            host synchronisation; NULL = none */
+                            host synchronisation; NULL = none, and a NULL entry skips
+                            that record */
     const float* amax_in; /* DELAYED only (required there): device fp32 statistic recorded by
                             an earlier call (its amax_out); may be the same memory as
                             amax_out, it is read before this call writes its own */

@@ -159,7 +159,8 @@ def scalify_matmul(a: ScaledArray, b: ScaledArray, out: ScaledArray, *, rescale:
     `amax_in` (RESCALE_DELAYED): one-element fp32 device tensor holding the
     statistic of an earlier call (its `amax_out`; may be the same tensor).
     `events`: an optional sequence of 3 torch.cuda.Event(enable_timing=True)
-    recorded before the GEMM kernel, after it and after the epilogue."""
+    recorded before the GEMM kernel, after it and after the epilogue (None
+    entries are skipped)."""
     lib = load_library()
     M, _ = a.shape
     _, N = b.shape
@@ -168,9 +169,9 @@ def scalify_matmul(a: ScaledArray, b: ScaledArray, out: ScaledArray, *, rescale:
     ev_arr = None
     if events is not None:
         for e in events:
-            if not e.cuda_event:       # torch creates its events lazily, on first record
+            if e is not None and not e.cuda_event:       # torch creates its events lazily, on first record
                 e.record(stream if stream is not None else torch.cuda.current_stream())
-        ev_arr = (ctypes.c_void_p * 3)(*[e.cuda_event for e in events])
+        ev_arr = (ctypes.c_void_p * 3)(*[e.cuda_event if e is not None else None for e in events])
     opts = CMatmulOpts(int(out.fmt), int(rescale), int(target_log2), int(bool(saturate)),
                        acc_out.data_ptr() if acc_out is not None else None,
                        amax_out.data_ptr() if amax_out is not None else None,

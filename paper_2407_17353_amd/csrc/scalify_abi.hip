@@ -161,12 +161,12 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
   p.ldc = out->ld;
   p.out_fmt = opts->out_dtype;
   hipEvent_t* ev = (hipEvent_t*)opts->events;
-  if (ev && hipEventRecord(ev[0], s) != hipSuccess) return SCALIFY_ERR_HIP;
+  if (ev && ev[0] && hipEventRecord(ev[0], s) != hipSuccess) return SCALIFY_ERR_HIP;
   if (M > 0 && N > 0) {
     if (launch_gemm(p, a->trans != 0, b->trans != 0, a->dtype, b->dtype, epi, s) != hipSuccess)
       return SCALIFY_ERR_HIP;
   }
-  if (ev && hipEventRecord(ev[1], s) != hipSuccess) return SCALIFY_ERR_HIP;
+  if (ev && ev[1] && hipEventRecord(ev[1], s) != hipSuccess) return SCALIFY_ERR_HIP;
   if (delayed) {
     // The statistic this call records for the next one.
     if (opts->amax_out && launch_finalize_amax(hdr, e_c, opts->amax_out, s) != hipSuccess)
@@ -191,7 +191,7 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
     if (launch_epilogue_cast(q, epi == EPI_INTER32, opts->out_dtype, s) != hipSuccess)
       return SCALIFY_ERR_HIP;
   }
-  if (ev && hipEventRecord(ev[2], s) != hipSuccess) return SCALIFY_ERR_HIP;
+  if (ev && ev[2] && hipEventRecord(ev[2], s) != hipSuccess) return SCALIFY_ERR_HIP;
   return SCALIFY_OK;
 }
 
