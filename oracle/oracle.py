@@ -13,6 +13,8 @@ Every function states the passage of the paper it follows:
     rebalance_scale (Section 3.3, Algorithm 4).
   * set_scaling / get_data_and_scale (Section 3.1); casts act on data only
     (Appendix A).
+  * scaled add (Algorithm 3: sqrt of the sum of squared scales, rounded down)
+    and activations f(x) = x * g(x) with the scale unchanged (Appendix C.1).
 
 Parity pins for every function live in tests/test_oracle_pins.py.
 """
@@ -26,6 +28,7 @@ import numpy as np
 
 E4M3, E5M2, F16, F32 = 0, 1, 2, 3
 RESCALE_NONE, RESCALE_AMAX, RESCALE_DELAYED = 0, 1, 2
+ACT_NONE, ACT_RELU, ACT_GELU_TANH, ACT_SILU = 0, 1, 2, 3
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "scalify_oracle.c")
@@ -79,6 +82,16 @@ def _load():
     lib.or_set_scaling.argtypes = [c_int, vp, c_i64, c_f32, c_i32, c_int, c_int, vp]
     lib.or_set_scaling.restype = c_int
     lib.or_cast_data.argtypes = [c_int, vp, c_i64, c_int, c_int, vp]
+    lib.or_gate.argtypes = [c_int, c_f64]
+    lib.or_gate.restype = c_f64
+    lib.or_add_scale_log2.argtypes = [c_i32, c_i32]
+    lib.or_add_scale_log2.restype = c_i32
+    lib.or_fused_pre.argtypes = [vp, c_i64, c_i64, c_f32, c_f32, c_i64, vp, c_int, c_i64, c_f32,
+                                 c_int, vp, vp, ctypes.POINTER(c_i32), ctypes.POINTER(c_i32)]
+    lib.or_fused_pre.restype = c_int
+    lib.or_finish_pre.argtypes = [vp, c_i64, c_i32, c_i32, c_int, c_i32, c_f32, c_int, c_int, vp,
+                                  ctypes.POINTER(c_f32)]
+    lib.or_finish_pre.restype = c_i32
     lib.or_init()
     _lib = lib
     return lib
@@ -217,6 +230,76 @@ def matmul(A, fa, ta, s_a, B, fb, tb, s_b, mode=RESCALE_AMAX, target_log2=0, sat
     K = A.shape[0] if ta else A.shape[1]
     codes, e_out, amax = matmul_epilogue(acc, s_a, s_b, K, mode, target_log2, saturate, out_fmt)
     return codes, e_out, amax, acc
+
+
+# --------------------------------------------------------------------------- fused add / activation
+
+def gate(act: int, x: float) -> float:
+    """Gating function g of f(x) = x * g(x) (Appendix C.1), fp64."""
+    return float(_load().or_gate(int(act), float(x)))
+
+
+def add_scale_log2(e1: int, e2: int) -> int:
+    """Scale exponent of a scaled add (Algorithm 3): sqrt(s1^2 + s2^2)
+    rounded down to a power of two."""
+    return int(_load().or_add_scale_log2(int(e1), int(e2)))
+
+
+def fused_pre(acc: np.ndarray, s_a: float, s_b: float, K: int, residual=None,
+              act: int = ACT_NONE):
+    """Pre-cast value of the matmul epilogue with a fused scaled add and
+    activation (Algorithm 3 add rule, Appendix C.1 activation rule).
+
+    residual: None or (codes, fmt, scale): codes [M,N] or [1,N] (one row
+    repeated, a bias) of format fmt with scalar scale `scale`.
+    Returns (w, y64, e_w, e_cc): w fp32 [M,N] with true value w * 2^e_w,
+    y64 the fp64 value before w's last rounding, and e_cc such that the
+    rescale statistic is taken over w * 2^-e_cc."""
+    lib = _load()
+    acc = np.ascontiguousarray(acc, dtype=np.float32)
+    M, N = acc.shape
+    w = np.empty((M, N), dtype=np.float32)
+    y64 = np.empty((M, N), dtype=np.float64)
+    e_w = ctypes.c_int32(0)
+    e_cc = ctypes.c_int32(0)
+    if residual is None:
+        rc = lib.or_fused_pre(_ptr(acc), M, N, s_a, s_b, int(K), None, 0, 0, 1.0, int(act),
+                              _ptr(w), _ptr(y64), ctypes.byref(e_w), ctypes.byref(e_cc))
+    else:
+        codes, fmt, scale = residual
+        codes = np.ascontiguousarray(codes, dtype=_code_dtype(fmt))
+        assert codes.shape in ((M, N), (1, N)), codes.shape
+        ld = 0 if codes.shape[0] == 1 and M != 1 else N
+        rc = lib.or_fused_pre(_ptr(acc), M, N, s_a, s_b, int(K), _ptr(codes), int(fmt), ld,
+                              float(scale), int(act), _ptr(w), _ptr(y64), ctypes.byref(e_w),
+                              ctypes.byref(e_cc))
+    if rc != 0:
+        raise ValueError("scales must be finite powers of two")
+    return w, y64, int(e_w.value), int(e_cc.value)
+
+
+def finish_pre(w: np.ndarray, e_w: int, e_cc: int, mode: int = RESCALE_AMAX, target_log2: int = 0,
+               amax_in: float = 0.0, saturate: bool = True, out_fmt: int = E4M3):
+    """Rescale (Section 3.3: amax, or the delayed statistic amax_in) and cast
+    (Section 2, stage 2) of pre-cast values w whose true value is w * 2^e_w.
+    Returns (codes, e_out, amax) with amax = max |w * 2^-e_cc| (non-NaN)."""
+    lib = _load()
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    out = np.empty(w.shape, dtype=_code_dtype(out_fmt))
+    amax = ctypes.c_float(0)
+    e_out = lib.or_finish_pre(_ptr(w), w.size, int(e_w), int(e_cc), int(mode), int(target_log2),
+                              float(amax_in), int(bool(saturate)), int(out_fmt), _ptr(out),
+                              ctypes.byref(amax))
+    return out, int(e_out), float(amax.value)
+
+
+def matmul_epilogue_fused(acc, s_a, s_b, K, residual=None, act=ACT_NONE, mode=RESCALE_AMAX,
+                          target_log2=0, amax_in=0.0, saturate=True, out_fmt=E4M3):
+    """Matmul epilogue with the fused scaled add and activation, then the
+    rescale and cast. Returns (codes, e_out, amax, w, y64)."""
+    w, y64, e_w, e_cc = fused_pre(acc, s_a, s_b, K, residual, act)
+    codes, e_out, amax = finish_pre(w, e_w, e_cc, mode, target_log2, amax_in, saturate, out_fmt)
+    return codes, e_out, amax, w, y64
 
 
 # --------------------------------------------------------------------------- rescale / cast

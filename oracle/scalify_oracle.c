@@ -508,3 +508,126 @@ void or_cast_data(int in_fmt, const void* in, int64_t n, int sat, int out_fmt, v
     }
     free(v);
 }
+
+/* ------------------------------------------------------------------------ */
+/* Scaled add and activation applied to the matmul output, before the        */
+/* rescale and cast (add rule: Section 3.2 / Algorithm 3; activation rule:  */
+/* Appendix C.1).                                                            */
+/* ------------------------------------------------------------------------ */
+
+enum { OR_ACT_NONE = 0, OR_ACT_RELU = 1, OR_ACT_GELU_TANH = 2, OR_ACT_SILU = 3 };
+
+/* Gating function g of an activation written f(x) = x * g(x), with g -> 0 at
+ * -inf and g -> 1 at +inf (Appendix C.1), evaluated in fp64:
+ *   relu: g = 1 for x > 0, else 0;
+ *   gelu, tanh form: g = (1 + tanh(sqrt(2/pi) * (x + 0.044715 x^3))) / 2;
+ *   silu (swish): g = 1 / (1 + exp(-x)).
+ * Any other act: g = 1 (identity). */
+double or_gate(int act, double x)
+{
+    switch (act) {
+    case OR_ACT_RELU:
+        return x > 0.0 ? 1.0 : 0.0;
+    case OR_ACT_GELU_TANH:
+        return 0.5 * (1.0 + tanh(sqrt(2.0 / M_PI) * (x + 0.044715 * x * x * x)));
+    case OR_ACT_SILU:
+        return 1.0 / (1.0 + exp(-x));
+    default:
+        return 1.0;
+    }
+}
+
+/* Output scale exponent of the scaled add (Algorithm 3): for independent
+ * unit-scaled operands the sum's standard deviation is sqrt(s_1^2 + s_2^2);
+ * like every scale it is rounded down to a power of two. */
+int32_t or_add_scale_log2(int32_t e1, int32_t e2)
+{
+    return or_floor_log2(sqrt(ldexp(1.0, 2 * e1) + ldexp(1.0, 2 * e2)));
+}
+
+/* Pre-cast value w[i] of the fused matmul epilogue, whose true value is
+ * w * 2^(*e_w); the data whose statistic the rescale gathers is
+ * w * 2^-(*e_cc).
+ *   - no residual: w = acc (true value acc * 2^(e_a+e_b)), e_cc = e_c: the
+ *     matmul's propagated data is acc * 2^-e_c (Section 3.2);
+ *   - residual R (codes res[i*res_ld + j], format res_fmt, scale s_res = 2^q;
+ *     res_ld = 0 repeats one row): scaled add of the matmul output
+ *     (scale 2^(e_a+e_b+e_c)) and R, e_w = add-rule exponent, e_cc = 0,
+ *     w = fl32(fl32(acc * 2^(e_a+e_b-e_w)) + fl32(r * 2^(q-e_w))): each
+ *     power-of-two product exact unless it underflows, one rounding of the sum;
+ *   - activation act (after the add, scale unchanged, Appendix C.1):
+ *     w = fl32(w * g(w * 2^e_w)).
+ * y64[i] (optional) receives the unrounded fp64 value before that last
+ * rounding (w itself without an activation).
+ * Returns 0, or -1 on a scale that is not a finite power of two. */
+int or_fused_pre(const float* acc, int64_t M, int64_t N, float s_a, float s_b, int64_t K,
+                 const void* res, int res_fmt, int64_t res_ld, float s_res, int act,
+                 float* w, double* y64, int32_t* e_w_out, int32_t* e_cc_out)
+{
+    int ok_a = 1, ok_b = 1, ok_r = 1;
+    int32_t e_a = or_scale_exponent(s_a, &ok_a);
+    int32_t e_b = or_scale_exponent(s_b, &ok_b);
+    int32_t e_c = or_matmul_scale_log2(K);
+    int32_t q = res ? or_scale_exponent(s_res, &ok_r) : 0;
+    int32_t e_w, e_cc;
+    int64_t i, j;
+    if (!ok_a || !ok_b || !ok_r) return -1;
+    if (res) {
+        e_w = or_add_scale_log2(e_a + e_b + e_c, q);
+        e_cc = 0;
+    } else {
+        e_w = e_a + e_b;
+        e_cc = e_c;
+    }
+    for (i = 0; i < M; ++i) {
+        for (j = 0; j < N; ++j) {
+            int64_t k = i * N + j;
+            double y;
+            float v = acc[k];
+            if (res) {
+                int64_t rk = i * res_ld + j;
+                uint32_t c = res_fmt == OR_F16 ? ((const uint16_t*)res)[rk]
+                                               : ((const uint8_t*)res)[rk];
+                float r = (float)or_decode(res_fmt, c);
+                v = (float)((double)ldexpf(v, e_a + e_b - e_w) + (double)ldexpf(r, q - e_w));
+            }
+            y = (double)v;
+            if (act != OR_ACT_NONE) y = (double)v * or_gate(act, ldexp((double)v, e_w));
+            if (y64) y64[k] = y;
+            w[k] = (float)y;
+        }
+    }
+    *e_w_out = e_w;
+    *e_cc_out = e_cc;
+    return 0;
+}
+
+/* Rescale and cast of pre-cast values w (true value w * 2^e_w; statistic
+ * over the data w * 2^-e_cc), Section 3.3 and stage 2 of Section 2:
+ *   amax = max |w| over non-NaN elements (reported as amax * 2^-e_cc);
+ *   AMAX: e_r = floor(log2 amax) - e_cc - t (0 for 0, +Inf, all NaN);
+ *   DELAYED: e_r from stat_in as in finish(); NONE: e_r = 0;
+ *   e_out = clamp(e_w + e_cc + e_r); codes = cast(w * 2^(e_w - e_out)),
+ * one power-of-two shift of w, then one rounding. Returns e_out. */
+int32_t or_finish_pre(const float* w, int64_t n, int32_t e_w, int32_t e_cc, int mode, int32_t t,
+                      float stat_in, int sat, int out_fmt, void* out, float* amax_out)
+{
+    int any;
+    float amax = or_amax(w, n, &any);
+    int32_t e_r = 0, e_out, shift;
+    int64_t i;
+    if (mode == OR_RESCALE_AMAX && any && amax != 0.0f && !isinf(amax))
+        e_r = or_floor_log2((double)amax) - e_cc - t;
+    if (mode == OR_RESCALE_DELAYED) e_r = or_rescale_exponent(stat_in, !isnan(stat_in), t);
+    e_out = clamp_e8m0(e_w + e_cc + e_r);
+    shift = e_w - e_out;
+    grids_init();
+    if (amax_out) *amax_out = ldexpf(amax, -e_cc);
+    #pragma omp parallel for schedule(static)
+    for (i = 0; i < n; ++i) {
+        uint32_t c = or_cast(out_fmt, sat, ldexpf(w[i], shift));
+        if (out_fmt == OR_F16) ((uint16_t*)out)[i] = (uint16_t)c;
+        else ((uint8_t*)out)[i] = (uint8_t)c;
+    }
+    return e_out;
+}
