@@ -520,7 +520,9 @@ enum { OR_ACT_NONE = 0, OR_ACT_RELU = 1, OR_ACT_GELU_TANH = 2, OR_ACT_SILU = 3 }
 /* Gating function g of an activation written f(x) = x * g(x), with g -> 0 at
  * -inf and g -> 1 at +inf (Appendix C.1), evaluated in fp64:
  *   relu: g = 1 for x > 0, else 0;
- *   gelu, tanh form: g = (1 + tanh(sqrt(2/pi) * (x + 0.044715 x^3))) / 2;
+ *   gelu, tanh form: g = (1 + tanh(u)) / 2 with u = sqrt(2/pi) (x + 0.044715 x^3),
+ *     evaluated as the equal 1 / (1 + exp(-2u)): 1 + tanh(u) cancels for
+ *     u << 0, where the gate would lose all its digits;
  *   silu (swish): g = 1 / (1 + exp(-x)).
  * Any other act: g = 1 (identity). */
 double or_gate(int act, double x)
@@ -528,8 +530,10 @@ double or_gate(int act, double x)
     switch (act) {
     case OR_ACT_RELU:
         return x > 0.0 ? 1.0 : 0.0;
-    case OR_ACT_GELU_TANH:
-        return 0.5 * (1.0 + tanh(sqrt(2.0 / M_PI) * (x + 0.044715 * x * x * x)));
+    case OR_ACT_GELU_TANH: {
+        double u = sqrt(2.0 / M_PI) * (x + 0.044715 * x * x * x);
+        return 1.0 / (1.0 + exp(-2.0 * u));
+    }
     case OR_ACT_SILU:
         return 1.0 / (1.0 + exp(-x));
     default:

@@ -55,6 +55,30 @@ def test_gelu_tanh_form_approximates_the_exact_gelu_to_its_known_error():
     assert 4.6e-4 < err < 4.8e-4
 
 
+@pytest.mark.parametrize("act", [orc.ACT_GELU_TANH, orc.ACT_SILU])
+def test_smooth_gates_keep_their_digits_in_the_negative_tail(act):
+    """Against 60-digit decimal arithmetic (an independent evaluation of
+    (1 + tanh(u))/2 = e^u / (e^u + e^-u), and of 1 / (1 + e^-x)): fp64
+    relative accuracy (1e-13, the rounding of the argument amplified by
+    |2u| < 150) down to gates of 1e-30, where the naive 1 + tanh(u) would
+    have cancelled to 0."""
+    from decimal import Decimal, getcontext
+    getcontext().prec = 60
+    k = Decimal(2) / Decimal("3.14159265358979323846264338327950288419716939937510582097494")
+    k = k.sqrt()
+    for x in np.linspace(-12.0, 2.0, 141):
+        d = Decimal(float(x))
+        if act == orc.ACT_GELU_TANH:
+            u = k * (d + Decimal("0.044715") * d * d * d)
+            ref = u.exp() / (u.exp() + (-u).exp())
+        else:
+            ref = 1 / (1 + (-d).exp())
+        if ref < Decimal("1e-30"):
+            continue
+        got = Decimal(orc.gate(act, float(x)))
+        assert abs(got - ref) <= ref * Decimal("1e-13"), (x, got, ref)
+
+
 def test_relu_gate_is_the_step():
     for x in [1e-300, 0.5, 3.0, 1e300, float("inf")]:
         assert orc.gate(orc.ACT_RELU, x) == 1.0
