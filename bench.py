@@ -88,7 +88,7 @@ def copy_calibration(dev, nbytes=256 << 20, reps=5):
     del src, dst
 
 
-def time_case(case, steps, warmup, dev, ws=None, mode=None):
+def time_case(case, steps, warmup, dev, ws=None, mode=None, act=0, residual_seed=None):
     """Time `steps` scalify_matmul calls of one GemmCase. Returns a dict with
     ms per call (event-timed over the whole timed region), the mean and the
     p10/p50/p90 duration of the fused GEMM kernel (events recorded by the
@@ -97,7 +97,10 @@ def time_case(case, steps, warmup, dev, ws=None, mode=None):
     after the epilogue, the mean epilogue-cast duration. Only the GEMM is
     bracketed in the timed region because every recorded event costs the
     stream a few microseconds. mode RESCALE_DELAYED keeps the statistic in
-    one device word that every call reads and rewrites (model state)."""
+    one device word that every call reads and rewrites (model state).
+    act / residual_seed: fuse that activation and, when residual_seed is
+    given, the scaled add of a seeded E4M3 N(0,1) residual [M, N] (scale 2)
+    into the GEMM epilogue."""
     import torch
     from paper_2407_17353_amd import binding as sc
 
@@ -107,11 +110,18 @@ def time_case(case, steps, warmup, dev, ws=None, mode=None):
     a = sc.ScaledArray(A, case.fa, sc.scale_tensor(case.a_scale_log2, dev), case.ta)
     b = sc.ScaledArray(B, case.fb, sc.scale_tensor(case.b_scale_log2, dev), case.tb)
     out = sc.empty_scaled(case.M, case.N, case.fout, dev)
-    need = sc.scalify_matmul_workspace_size(case.M, case.N, case.fout, mode)
+    fused = act != 0 or residual_seed is not None
+    need = sc.scalify_matmul_workspace_size_opts(case.M, case.N, case.fout, mode, fused)
     if ws is None or ws.numel() < need:
         ws = sc.workspace(need, dev)
     state = torch.zeros(1, dtype=torch.float32, device=dev)
     kw = {"amax_in": state, "amax_out": state} if mode == sc.RESCALE_DELAYED else {}
+    if fused:
+        kw["activation"] = act
+    if residual_seed is not None:
+        from paper_2407_17353_amd import workloads as wl
+        R = wl.fp8_normal((case.M, case.N), wl.E4M3, residual_seed, dev)
+        kw["residual"] = sc.ScaledArray(R, wl.E4M3, sc.scale_tensor(1, dev))
     stream = torch.cuda.current_stream()
     for _ in range(warmup):
         sc.scalify_matmul(a, b, out, rescale=mode, ws=ws, **kw)
@@ -235,6 +245,17 @@ def main():
         "ms_per_step": round(rd["ms_per_step"], 4),
         "pct_of_peak": round(100.0 * flops / (rd["ms_per_step"] * 1e-3) / 1e12 / PEAK_FP8_TFLOPS, 2),
         "gemm_kernel_us": round(rd["gemm_ms"] * 1e3, 2)}
+    # The same workload with the scaled add of a residual and GELU fused into
+    # the epilogue (Algorithm 3 add rule, Appendix C.1), dynamic and delayed.
+    line["fused_add_gelu"] = {}
+    for name, m in (("amax", sc.RESCALE_AMAX), ("delayed", sc.RESCALE_DELAYED)):
+        rf, ws = time_case(case, args.steps // 2, args.warmup // 2, dev, ws, mode=m,
+                           act=sc.ACT_GELU_TANH, residual_seed=wl.seed_of(4, 30))
+        line["fused_add_gelu"][name] = {
+            "value": round(flops / (rf["ms_per_step"] * 1e-3) / 1e12, 2), "unit": "TFLOP/s",
+            "ms_per_step": round(rf["ms_per_step"], 4),
+            "gemm_kernel_us": round(rf["gemm_ms"] * 1e3, 2),
+            "epilogue_cast_us": round(rf["cast_ms"] * 1e3, 2) if m == sc.RESCALE_AMAX else None}
     if args.sweep:
         sweep = []
         for cfg, cases in wl.all_configs().items():

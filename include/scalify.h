@@ -68,6 +68,16 @@ typedef enum {
     SCALIFY_RESCALE_DELAYED = 2 /* delayed rescale: from the amax an earlier call recorded */
 } scalify_rescale_mode;
 
+/* Activation applied by the matmul epilogue (Appendix C.1): f(x) = x * g(x)
+ * with a gate g -> 0 at -inf and -> 1 at +inf; on a ScaledArray the scale
+ * is kept and the data becomes X_d * g(X_d * X_s). */
+typedef enum {
+    SCALIFY_ACT_NONE = 0,
+    SCALIFY_ACT_RELU = 1,      /* g = 1 for x > 0, else 0 */
+    SCALIFY_ACT_GELU_TANH = 2, /* g = (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3))) / 2 */
+    SCALIFY_ACT_SILU = 3       /* g = 1 / (1 + exp(-x)) (swish) */
+} scalify_activation;
+
 /* A ScaledArray (Section 2, Section 3.1): value = decode(data) * (*scale).
  * Logical shape rows x cols.
  *   trans = 0: element (r, c) is stored at data[r * ld + c]  (ld >= cols)
@@ -91,7 +101,9 @@ typedef struct {
     int32_t target_log2; /* t: AMAX puts the rescaled amax in [2^t, 2^(t+1)); default 0 */
     int32_t saturate;    /* 1: overflow and +-Inf -> +-max; 0: E4M3 -> NaN, E5M2/F16 -> +-Inf */
     float* acc_out;      /* optional device [M][N] fp32: the raw accumulator sum_k a_ik b_kj */
-    float* amax_out;     /* optional device fp32: amax of acc * 2^-e_c over non-NaN elements */
+    float* amax_out;     /* optional device fp32: amax of acc * 2^-e_c over non-NaN elements
+                            (with a fused add or activation: of the data the statistic is
+                            gathered over, see scalify_matmul) */
     void** events;       /* optional host array of 3 hipEvent_t recorded on the stream: before
                             the GEMM kernel, after it, and after the epilogue cast (DELAYED:
                             after the amax write-back) -- timing of the fused GEMM without
@@ -100,6 +112,16 @@ typedef struct {
     const float* amax_in; /* DELAYED only (required there): device fp32 statistic recorded by
                             an earlier call (its amax_out); may be the same memory as
                             amax_out, it is read before this call writes its own */
+    const scalify_scaled_array* residual; /* optional: R added to the product by the scaled
+                            add rule before the activation (see scalify_matmul); E4M3, E5M2 or
+                            F16, rows = M, cols = N, trans = 0, 16-byte aligned, ld a multiple
+                            of 16 elements (8 for F16) and >= N, or ld = 0: one row added to
+                            every row (a bias). It may be the very same matrix as out (same
+                            data, dtype and ld) but must not otherwise overlap it. NULL = none */
+    int32_t activation;  /* scalify_activation applied after the add; NONE = 0 */
+    float* pre_out;      /* optional validation output: device fp32 [M][N], the value w the
+                            rescale and cast see (after the add and the activation), whose
+                            true value is w * 2^e_w (e_w as in scalify_matmul) */
 } scalify_matmul_opts;
 
 /* Exponent e_c of the matmul scale rule (Section 3.2, Algorithm 3): the
@@ -113,6 +135,12 @@ int32_t scalify_matmul_scale_log2(int64_t K);
  * elements; 2 bytes per element for FP8 outputs, 4 for FP16). DELAYED needs
  * the header only. Returns 0 for invalid arguments. */
 size_t scalify_matmul_workspace_size(int64_t M, int64_t N, int32_t out_dtype, int32_t rescale);
+
+/* Workspace bytes of a scalify_matmul call with these options: as above, but
+ * a call that fuses a residual add or an activation, or asks for pre_out,
+ * keeps an fp32 intermediate (4 bytes per element for every output type).
+ * Returns 0 for invalid arguments or a NULL opts. */
+size_t scalify_matmul_workspace_size_opts(int64_t M, int64_t N, const scalify_matmul_opts* opts);
 
 /* Scaled matmul on ScaledArray operands (Section 3.2, Algorithm 3; FP8
  * matmul with mixed input formats and higher-precision accumulation,
@@ -133,11 +161,28 @@ size_t scalify_matmul_workspace_size(int64_t M, int64_t N, int32_t out_dtype, in
  *               when opts.saturate), *out.scale = 2^e_out
  * so that dec(out) * s_out = s_a * s_b * acc up to the final rounding.
  *
+ * Fused scaled add and activation (opts.residual, opts.activation): the
+ * epilogue first forms w, whose true value is w * 2^e_w, then rescales and
+ * casts w in place of acc:
+ *   no residual: w = acc, e_w = e_a + e_b, statistic over w * 2^-e_c;
+ *   residual R (scale 2^q): scaled add (Algorithm 3) of the product, whose
+ *     propagated scale is 2^(e_a+e_b+e_c), and R: the output scale is
+ *     sqrt(s_p^2 + s_r^2) rounded down to a power of two, i.e. e_w =
+ *     max(e_a + e_b + e_c, q); w = fl32(acc * 2^(e_a+e_b-e_w) + dec(R) * 2^(q-e_w))
+ *     (one rounding of the sum), statistic over w;
+ *   activation (Appendix C.1, after the add): w = fl32(w * g(w * 2^e_w)),
+ *     scale unchanged; relu is exact, gelu and silu are evaluated in fp32
+ *     (within a few ulp of the exact gate).
+ *   Then e_out = clamp(e_w + (e_c, or 0 with a residual) + e_r) with e_r from
+ *   the statistic of w (AMAX) or from amax_in (DELAYED), and
+ *   out.data = RNE(w * 2^(e_w - e_out)); amax_out is that statistic.
+ *
  * a: M x K, b: K x N, out: M x N. a and b are E4M3 or E5M2 in any mix and
  * either storage order (trans 0/1). out.trans must be 0 and out.dtype must
  * equal opts->out_dtype. All data pointers 16-byte aligned, every ld a
  * multiple of 16 elements (8 for an FP16 out). workspace: device memory of
- * at least scalify_matmul_workspace_size(M, N, ...) bytes, 256-byte aligned,
+ * at least scalify_matmul_workspace_size_opts(M, N, opts) bytes (for a call
+ * with nothing fused: scalify_matmul_workspace_size(M, N, ...)), 256-byte aligned,
  * not shared with a concurrent call. Determinism: reruns are bit-identical.
  * M, N or K may be 0 (K = 0 gives an all-zero output). */
 scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scaled_array* b,

@@ -17,6 +17,7 @@ import torch
 
 E4M3, E5M2, F16, F32 = 0, 1, 2, 3
 RESCALE_NONE, RESCALE_AMAX, RESCALE_DELAYED = 0, 1, 2
+ACT_NONE, ACT_RELU, ACT_GELU_TANH, ACT_SILU = 0, 1, 2, 3
 
 STATUS_NAMES = {0: "SCALIFY_OK", 1: "SCALIFY_ERR_NULL", 2: "SCALIFY_ERR_DTYPE",
                 3: "SCALIFY_ERR_SHAPE", 4: "SCALIFY_ERR_LAYOUT", 5: "SCALIFY_ERR_ALIGN",
@@ -45,10 +46,13 @@ class CMatmulOpts(ctypes.Structure):
     _fields_ = [("out_dtype", ctypes.c_int32), ("rescale", ctypes.c_int32),
                 ("target_log2", ctypes.c_int32), ("saturate", ctypes.c_int32),
                 ("acc_out", ctypes.c_void_p), ("amax_out", ctypes.c_void_p),
-                ("events", ctypes.c_void_p), ("amax_in", ctypes.c_void_p)]
+                ("events", ctypes.c_void_p), ("amax_in", ctypes.c_void_p),
+                ("residual", ctypes.POINTER(CScaledArray)), ("activation", ctypes.c_int32),
+                ("pre_out", ctypes.c_void_p)]
 
 
-EXPORTED = ("scalify_matmul_scale_log2", "scalify_matmul_workspace_size", "scalify_matmul",
+EXPORTED = ("scalify_matmul_scale_log2", "scalify_matmul_workspace_size",
+            "scalify_matmul_workspace_size_opts", "scalify_matmul",
             "scalify_rescale_workspace_size", "scalify_rescale", "scalify_cast",
             "scalify_set_scaling", "scalify_status_string")
 
@@ -70,6 +74,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.scalify_matmul_scale_log2.restype = i32
     lib.scalify_matmul_workspace_size.argtypes = [i64, i64, i32, i32]
     lib.scalify_matmul_workspace_size.restype = ctypes.c_size_t
+    lib.scalify_matmul_workspace_size_opts.argtypes = [i64, i64, P(CMatmulOpts)]
+    lib.scalify_matmul_workspace_size_opts.restype = ctypes.c_size_t
     lib.scalify_matmul.argtypes = [P(CScaledArray), P(CScaledArray), P(CScaledArray),
                                    P(CMatmulOpts), vp, ctypes.c_size_t, vp]
     lib.scalify_matmul.restype = ctypes.c_int
@@ -141,6 +147,15 @@ def scalify_matmul_workspace_size(M: int, N: int, out_fmt: int, rescale: int = R
     return int(load_library().scalify_matmul_workspace_size(M, N, out_fmt, rescale))
 
 
+def scalify_matmul_workspace_size_opts(M: int, N: int, out_fmt: int, rescale: int = RESCALE_AMAX,
+                                       fused: bool = False) -> int:
+    """Workspace bytes of a call with (fused=True) or without a fused
+    residual add, activation or pre_out export."""
+    opts = CMatmulOpts(int(out_fmt), int(rescale), 0, 1, None, None, None, None, None,
+                       ACT_RELU if fused else ACT_NONE, None)
+    return int(load_library().scalify_matmul_workspace_size_opts(M, N, ctypes.byref(opts)))
+
+
 def scalify_rescale_workspace_size(n: int) -> int:
     return int(load_library().scalify_rescale_workspace_size(n))
 
@@ -153,19 +168,23 @@ def workspace(nbytes: int, device) -> torch.Tensor:
 def scalify_matmul(a: ScaledArray, b: ScaledArray, out: ScaledArray, *, rescale: int = RESCALE_AMAX,
                    target_log2: int = 0, saturate: bool = True, acc_out: torch.Tensor = None,
                    amax_out: torch.Tensor = None, amax_in: torch.Tensor = None,
+                   residual: "ScaledArray" = None, activation: int = ACT_NONE,
+                   pre_out: torch.Tensor = None,
                    ws: torch.Tensor = None, stream=None, events=None) -> None:
     """Scaled matmul (Section 3.2) with the fused dynamic or delayed rescale
     and cast (Section 3.3); see scalify_matmul in include/scalify.h.
     `amax_in` (RESCALE_DELAYED): one-element fp32 device tensor holding the
     statistic of an earlier call (its `amax_out`; may be the same tensor).
+    `residual`: ScaledArray [M, N] added by the scaled add rule before the
+    `activation` (ACT_*); a row broadcast as `bias.expand(M, N)` (stride 0)
+    adds one row to every row. `pre_out`: fp32 [M, N] device tensor that
+    receives the pre-cast value w (validation).
     `events`: an optional sequence of 3 torch.cuda.Event(enable_timing=True)
     recorded before the GEMM kernel, after it and after the epilogue (None
     entries are skipped)."""
     lib = load_library()
     M, _ = a.shape
     _, N = b.shape
-    if ws is None:
-        ws = workspace(scalify_matmul_workspace_size(M, N, out.fmt, rescale), a.data.device)
     ev_arr = None
     if events is not None:
         for e in events:
@@ -176,7 +195,14 @@ def scalify_matmul(a: ScaledArray, b: ScaledArray, out: ScaledArray, *, rescale:
                        acc_out.data_ptr() if acc_out is not None else None,
                        amax_out.data_ptr() if amax_out is not None else None,
                        ctypes.cast(ev_arr, ctypes.c_void_p) if ev_arr is not None else None,
-                       amax_in.data_ptr() if amax_in is not None else None)
+                       amax_in.data_ptr() if amax_in is not None else None,
+                       None, int(activation), pre_out.data_ptr() if pre_out is not None else None)
+    cr = residual.c_struct() if residual is not None else None
+    if cr is not None:
+        opts.residual = ctypes.pointer(cr)
+    if ws is None:
+        ws = workspace(lib.scalify_matmul_workspace_size_opts(M, N, ctypes.byref(opts)),
+                       a.data.device)
     ca, cb, co = a.c_struct(), b.c_struct(), out.c_struct()
     st = lib.scalify_matmul(ctypes.byref(ca), ctypes.byref(cb), ctypes.byref(co), ctypes.byref(opts),
                             ws.data_ptr(), ws.numel(), _stream_handle(stream))

@@ -154,6 +154,13 @@ __device__ __forceinline__ uint32_t cast4_fp8_hw(uint32_t u0, uint32_t u1, uint3
 
 __device__ __forceinline__ bool is_nan_bits(uint32_t u) { return (u & 0x7FFFFFFFu) > 0x7F800000u; }
 
+// NaN, or a nonzero fp32 subnormal: inputs that take the exact integer cast
+// instead of the hardware conversions.
+__device__ __forceinline__ bool needs_exact_bits(uint32_t u) {
+  const uint32_t e = u & 0x7F800000u;
+  return (e == 0x7F800000u || e == 0u) && (u & 0x7FFFFFu) != 0u;
+}
+
 // Exact fp32 bits of an FP8 / FP16 code (all FP8 and FP16 values are fp32).
 template <int F>
 __device__ __forceinline__ uint32_t decode_bits(uint32_t c);

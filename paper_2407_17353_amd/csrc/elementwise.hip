@@ -31,28 +31,37 @@ hipError_t launch_prologue(uint32_t* hdr, const float* s0, const float* s1, hipS
   return hipGetLastError();
 }
 
-// Delayed rescale (Section 3.3): the rebalance uses the statistic an earlier
-// call recorded, so the output scale is known before the GEMM runs.
-__global__ void prologue_delayed_kernel(uint32_t* hdr, const float* s0, const float* s1,
-                                        const float* amax_in, int e_c, int target,
-                                        float* out_scale) {
+// Matmul prologue: the scale exponent e_w of the pre-cast value (scaled add
+// rule of Algorithm 3 with a residual) and, for the delayed rescale
+// (Section 3.3), the output scale from the statistic an earlier call
+// recorded, so that the GEMM can cast directly.
+__global__ void matmul_prologue_kernel(uint32_t* hdr, MatmulPrologue q) {
   if (threadIdx.x == 0) {
-    const int e_ab = pow2_exponent(s0) + pow2_exponent(s1);
-    const uint32_t stat = __float_as_uint(*amax_in) & 0x7FFFFFFFu;  // |statistic|
-    const int e_r = rescale_exponent(stat, target);  // 0 for 0, Inf, NaN
-    const int e_out = clamp_e8m0(e_ab + e_c + e_r);
+    const int e_ab = pow2_exponent(q.s0) + pow2_exponent(q.s1);
+    int e_w = e_ab, e_cc = q.e_c;
+    if (q.residual) {
+      // sqrt(2^(2 e_p) + 2^(2 e_q)) rounded down to a power of two is the
+      // larger of the two scales.
+      const int e_q = pow2_exponent(q.s_res);
+      e_w = max(e_ab + q.e_c, e_q);
+      e_cc = 0;
+      hdr[3] = (uint32_t)(e_ab - e_w);
+      hdr[4] = (uint32_t)(e_q - e_w);
+    }
     hdr[0] = 0u;
-    hdr[1] = (uint32_t)e_ab;
-    hdr[2] = (uint32_t)(e_out - e_ab);
-    *out_scale = pow2_float(e_out);
+    hdr[1] = (uint32_t)e_w;
+    if (q.delayed) {
+      const uint32_t stat = __float_as_uint(*q.amax_in) & 0x7FFFFFFFu;  // |statistic|
+      const int e_r = rescale_exponent(stat, q.target);  // 0 for 0, Inf, NaN
+      const int e_out = clamp_e8m0(e_w + e_cc + e_r);
+      hdr[2] = (uint32_t)(e_out - e_w);
+      *q.out_scale = pow2_float(e_out);
+    }
   }
 }
 
-hipError_t launch_prologue_delayed(uint32_t* hdr, const float* s0, const float* s1,
-                                   const float* amax_in, int e_c, int target, float* out_scale,
-                                   hipStream_t s) {
-  hipLaunchKernelGGL(prologue_delayed_kernel, dim3(1), dim3(64), 0, s, hdr, s0, s1, amax_in, e_c,
-                     target, out_scale);
+hipError_t launch_matmul_prologue(uint32_t* hdr, const MatmulPrologue& q, hipStream_t s) {
+  hipLaunchKernelGGL(matmul_prologue_kernel, dim3(1), dim3(64), 0, s, hdr, q);
   return hipGetLastError();
 }
 
@@ -129,14 +138,15 @@ __device__ __forceinline__ void store1(void* base, int64_t e, uint32_t c) {
 
 // 16 fp32 values (bits) times 2^-shift -> 16 codes packed in 4 words (FP8)
 // or 8 words (FP16: two codes per word). FP8 uses the hardware conversion
-// when the scale fits and no value is NaN, else the integer cast.
+// when the scale fits and no value is NaN or an fp32 subnormal, else the
+// integer cast.
 template <int OUTF>
 __device__ __forceinline__ void encode16(const uint32_t (&u)[16], int shift, float scale, bool fast,
                                          bool sat, uint32_t (&w)[8]) {
   if (OUTF == kE4M3 || OUTF == kE5M2) {
     bool nan = false;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) nan |= is_nan_bits(u[i]);
+    for (int i = 0; i < 16; ++i) nan |= needs_exact_bits(u[i]);
     if (fast && !nan) {
 #pragma unroll
       for (int q = 0; q < 4; ++q)
@@ -177,8 +187,8 @@ __device__ __forceinline__ uint32_t word_code(const uint32_t (&w)[8], int i) {
 
 template <int INTER32, int OUTF>
 __global__ __launch_bounds__(EW_THREADS) void epilogue_cast_kernel(EpilogueParams p) {
-  const uint32_t amax_raw = p.hdr[0];  // max |acc| bits
-  const int e_ab = (int)p.hdr[1];
+  const uint32_t amax_raw = p.hdr[0];  // max |w| bits
+  const int e_ab = (int)p.hdr[1];      // e_w
   int e_r = 0;
   if (p.mode == 1 && amax_raw != 0u && amax_raw < 0x7F800000u)
     e_r = floor_log2_bits(amax_raw) - p.e_c - p.target;
@@ -229,8 +239,12 @@ hipError_t launch_epilogue_cast(const EpilogueParams& p, int inter32, int out_dt
   const int gx = (cpr + EW_THREADS - 1) / EW_THREADS;
   const int gy = p.M < 1 ? 1 : (p.M > 65535 ? 65535 : p.M);
   const dim3 g(gx < 1 ? 1 : gx, gy), b(EW_THREADS);
-  if (inter32) {
+  if (inter32 && out_dtype == kF16) {
     hipLaunchKernelGGL((epilogue_cast_kernel<1, kF16>), g, b, 0, s, p);
+  } else if (inter32 && out_dtype == kE4M3) {
+    hipLaunchKernelGGL((epilogue_cast_kernel<1, kE4M3>), g, b, 0, s, p);
+  } else if (inter32) {
+    hipLaunchKernelGGL((epilogue_cast_kernel<1, kE5M2>), g, b, 0, s, p);
   } else if (out_dtype == kE4M3) {
     hipLaunchKernelGGL((epilogue_cast_kernel<0, kE4M3>), g, b, 0, s, p);
   } else {

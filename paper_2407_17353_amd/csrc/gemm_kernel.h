@@ -217,25 +217,27 @@ __device__ __forceinline__ void static_for(F&& f) {
   }
 }
 
-// Direct cast of 4 accumulator values (fp32 bits) times 2^-shift, for the
+// Direct cast of 4 pre-cast values (fp32 bits) times 2^-shift, for the
 // delayed rescale. Fast paths use the hardware conversions (callers check
-// that |shift| <= kFastShiftMax and that no value is NaN); the exact integer
-// casts are kept out of line.
+// that |shift| <= kFastShiftMax and that no value is NaN, nor, in the fused
+// kernels, an fp32 subnormal); the exact integer casts are kept out of line.
 __device__ __forceinline__ v2i cast4_f16_hw(uint32_t u0, uint32_t u1, uint32_t u2, uint32_t u3,
                                            float inv, bool sat) {
   // x * 2^-shift (inv = 2^-shift) is exact in fp32 unless it leaves the
   // fp32 normal range: above it the conversion overflows as the exact value
   // would, below it the value rounds to zero in FP16 either way.
   // v_cvt_f16_f32 then rounds to nearest even, keeping FP16 subnormals;
-  // overflow gives +-Inf, which saturation turns into +-max.
+  // overflow gives Inf, which saturation turns into max. The magnitude is
+  // converted and the sign put back: the compiler fuses the multiply and
+  // the conversion into an fma whose +0 addend would turn -0 into +0.
   uint32_t h[4];
   const uint32_t u[4] = {u0, u1, u2, u3};
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const _Float16 f = (_Float16)(__uint_as_float(u[i]) * inv);
+    const _Float16 f = (_Float16)(__uint_as_float(u[i] & 0x7FFFFFFFu) * inv);
     uint32_t b = (uint32_t)__builtin_bit_cast(uint16_t, f);
-    if (sat && (b & 0x7FFFu) == 0x7C00u) b -= 1u;  // +-Inf -> +-65504
-    h[i] = b;
+    if (sat && b == 0x7C00u) b = 0x7BFFu;  // Inf -> 65504
+    h[i] = b | ((u[i] >> 16) & 0x8000u);
   }
   return v2i{(int)(h[0] | (h[1] << 16)), (int)(h[2] | (h[3] << 16))};
 }
@@ -256,7 +258,96 @@ __device__ __attribute__((noinline)) uint32_t cast4_slow_fp8(int fmt, uint32_t u
          (cast_bits<kE5M2>(u2, shift, sat) << 16) | (cast_bits<kE5M2>(u3, shift, sat) << 24);
 }
 
-template <bool A_MN, bool B_KC, int FA, int FB, int EPI>
+// ---- fused epilogue: scaled add of a residual (Algorithm 3 rule) and an
+// activation f(x) = x * g(x) with the scale kept (Appendix C.1).
+
+// Raw residual codes at row m, columns n..n+3 (columns >= N are not read
+// and come back as 0): FP8 packs the 4 codes in c[0], FP16 two per word.
+__device__ __forceinline__ void load_residual_codes(const GemmParams& p, int m, int n,
+                                                    uint32_t (&c)[2]) {
+  const int64_t e = (int64_t)m * p.ldr + n;
+  c[0] = c[1] = 0u;
+  if (p.res_fmt == kF16) {
+    const uint16_t* q = (const uint16_t*)p.res + e;
+    if (n + 3 < p.N) {
+      const v2i w = *(const v2i*)q;
+      c[0] = (uint32_t)w.x;
+      c[1] = (uint32_t)w.y;
+    } else {
+      c[0] = q[0];
+      if (n + 1 < p.N) c[0] |= (uint32_t)q[1] << 16;
+      if (n + 2 < p.N) c[1] = q[2];
+    }
+  } else {
+    const uint8_t* q = (const uint8_t*)p.res + e;
+    if (n + 3 < p.N) {
+      c[0] = *(const uint32_t*)q;
+    } else {
+      c[0] = q[0];
+      if (n + 1 < p.N) c[0] |= (uint32_t)q[1] << 8;
+      if (n + 2 < p.N) c[0] |= (uint32_t)q[2] << 16;
+    }
+  }
+}
+
+// Residual codes decoded exactly to fp32.
+__device__ __forceinline__ v4f decode_residual4(int fmt, const uint32_t (&c)[2]) {
+  v4f r;
+  if (fmt == kF16) {
+    r[0] = __uint_as_float(decode_bits<kF16>(c[0] & 0xFFFFu));
+    r[1] = __uint_as_float(decode_bits<kF16>(c[0] >> 16));
+    r[2] = __uint_as_float(decode_bits<kF16>(c[1] & 0xFFFFu));
+    r[3] = __uint_as_float(decode_bits<kF16>(c[1] >> 16));
+  } else if (fmt == kE4M3) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) r[i] = __uint_as_float(decode_bits<kE4M3>((c[0] >> (8 * i)) & 0xFFu));
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) r[i] = __uint_as_float(decode_bits<kE5M2>((c[0] >> (8 * i)) & 0xFFu));
+  }
+  return r;
+}
+
+// Smooth gates in fp32: silu g(x) = 1 / (1 + e^-x); the tanh form of gelu
+// (1 + tanh(u)) / 2 with u = sqrt(2/pi) (x + 0.044715 x^3) is the same
+// sigmoid at 2u. Defined at +-Inf (1 and 0); NaN stays NaN. Within a few ulp
+// of the exact gate where it is a normal fp32 (below 2^-126 it may flush).
+__device__ __forceinline__ float smooth_gate(int act, float x) {
+  float t = x;
+  if (act == ACT_GELU_TANH) {
+    const float k0 = 1.5957691216057308f;   // 2 sqrt(2/pi)
+    const float k1 = 0.07135481627260025f;  // 2 sqrt(2/pi) * 0.044715
+    t = x * (k0 + k1 * (x * x));
+  }
+  return __builtin_amdgcn_rcpf(1.0f + expf(-t));
+}
+
+// w for 4 adjacent outputs: acc -> (scaled add of the residual codes rc0,
+// rc1 of format res_fmt when has_res) -> (activation act). sh_acc, sh_res:
+// power-of-two shifts of acc and of the residual into w's scale 2^e_w; the
+// gate sees the true value w * 2^e_w. Out of line: the epilogue calls it
+// once per 4 outputs, and one copy keeps the kernel's code small enough for
+// the instruction cache.
+__device__ __attribute__((noinline)) v4f fuse4(v4f v, uint32_t rc0, uint32_t rc1, int has_res,
+                                               int res_fmt, int act, int sh_acc, int sh_res,
+                                               int e_w) {
+  if (has_res) {
+    const uint32_t rc[2] = {rc0, rc1};
+    const v4f r = decode_residual4(res_fmt, rc);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = ldexpf(v[i], sh_acc) + ldexpf(r[i], sh_res);
+  }
+  if (act == ACT_RELU) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = v[i] * (v[i] > 0.0f ? 1.0f : 0.0f);
+  } else if (act != ACT_NONE) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = v[i] * smooth_gate(act, ldexpf(v[i], e_w));
+  }
+  return v;
+}
+
+template <bool A_MN, bool B_KC, int FA, int FB, int EPI, bool FUSE>
 __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
   __shared__ __attribute__((aligned(1024))) uint8_t sA0[TILE_BYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t sB0[TILE_BYTES];
@@ -416,12 +507,34 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
   const float hw_scale = fast ? pow2_float(shift) : 1.0f;
   const float hw_inv = fast ? pow2_float(-shift) : 1.0f;
   const bool sat = p.sat != 0;
+  // FUSE: the shifts of the scaled add and the scale exponent of w.
+  int f_sh_acc = 0, f_sh_res = 0, f_ew = 0;
+  // FUSE: the residual codes of all the wave's outputs, loaded up front so
+  // that their memory latencies overlap.
+  uint32_t rcodes[FUSE ? MI : 1][FUSE ? NI : 1][2] = {};
+  if constexpr (FUSE) {
+    f_ew = (int)__builtin_amdgcn_readfirstlane(p.hdr[1]);
+    if (p.res) {
+      f_sh_acc = (int)__builtin_amdgcn_readfirstlane(p.hdr[3]);
+      f_sh_res = (int)__builtin_amdgcn_readfirstlane(p.hdr[4]);
+      static_for<0, MI * NI>([&](auto I) {
+        constexpr int mi = decltype(I)::value / NI, ni = decltype(I)::value % NI;
+        const int m = mb + 16 * mi;
+        const int n = nb + 16 * ni;
+        if (m < M && n < N) load_residual_codes(p, m, n, rcodes[mi][ni]);
+      });
+    }
+  }
   static_for<0, MI * NI>([&](auto I) {
     constexpr int mi = decltype(I)::value / NI, ni = decltype(I)::value % NI;
     const int m = mb + 16 * mi;
     const int n = nb + 16 * ni;
-    const v4f v = acc[mi][ni];
     if (m < M && n < N) {
+      v4f v = acc[mi][ni];
+      if constexpr (FUSE) {
+        const uint32_t(&rc)[2] = rcodes[FUSE ? mi : 0][FUSE ? ni : 0];
+        v = fuse4(v, rc[0], rc[1], p.res != nullptr, p.res_fmt, p.act, f_sh_acc, f_sh_res, f_ew);
+      }
       lmax = fmaxf(lmax, fabsf(v[0]));
       if (n + 1 < N) lmax = fmaxf(lmax, fabsf(v[1]));
       if (n + 2 < N) lmax = fmaxf(lmax, fabsf(v[2]));
@@ -440,7 +553,10 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
         // Hardware conversions unless a lane of the wave holds a NaN or the
         // shift is out of their range (then the exact integer cast, out of
         // line: it is rare and large).
-        const bool nan = is_nan_bits(u0) || is_nan_bits(u1) || is_nan_bits(u2) || is_nan_bits(u3);
+        const bool nan = FUSE ? (needs_exact_bits(u0) || needs_exact_bits(u1) ||
+                                 needs_exact_bits(u2) || needs_exact_bits(u3))
+                              : (is_nan_bits(u0) || is_nan_bits(u1) || is_nan_bits(u2) ||
+                                 is_nan_bits(u3));
         const bool hw = fast && !__any(nan);
         if (p.out_fmt == kF16) {
           v2i w;
@@ -476,11 +592,21 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
         }
       }
       if (p.acc_out) {
+        const v4f a = acc[mi][ni];
         float* q = p.acc_out + (int64_t)m * N + n;
-        q[0] = v[0];
-        if (n + 1 < N) q[1] = v[1];
-        if (n + 2 < N) q[2] = v[2];
-        if (n + 3 < N) q[3] = v[3];
+        q[0] = a[0];
+        if (n + 1 < N) q[1] = a[1];
+        if (n + 2 < N) q[2] = a[2];
+        if (n + 3 < N) q[3] = a[3];
+      }
+      if constexpr (FUSE) {
+        if (p.pre_out) {
+          float* q = p.pre_out + (int64_t)m * N + n;
+          q[0] = v[0];
+          if (n + 1 < N) q[1] = v[1];
+          if (n + 2 < N) q[2] = v[2];
+          if (n + 3 < N) q[3] = v[3];
+        }
       }
     }
   });
@@ -497,9 +623,35 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
   }
 }
 
-// Launch of one (layout, format, epilogue) family; defined per layout in
-// gemm_<layout>.hip so that the instantiations compile in parallel.
-template <bool A_MN, bool B_KC>
+// Launch of one (layout, fused or not) family over the format pairs and
+// epilogues; each family is instantiated in a source file of its own
+// (gemm_<layout>[_fused].hip) so that they compile in parallel.
+template <bool A_MN, bool B_KC, bool FUSE>
 hipError_t launch_layout(const GemmParams& p, int fa, int fb, int epi, hipStream_t s);
+
+template <bool A_MN, bool B_KC, bool FUSE, int FA, int FB>
+hipError_t launch_fmt(const GemmParams& p, int epi, hipStream_t s) {
+  const dim3 grid(p.tiles_m * p.tiles_n), block(NTHR);
+  switch (epi) {
+    case EPI_INTER16:
+      hipLaunchKernelGGL((gemm_kernel<A_MN, B_KC, FA, FB, EPI_INTER16, FUSE>), grid, block, 0, s, p);
+      break;
+    case EPI_INTER32:
+      hipLaunchKernelGGL((gemm_kernel<A_MN, B_KC, FA, FB, EPI_INTER32, FUSE>), grid, block, 0, s, p);
+      break;
+    default:
+      hipLaunchKernelGGL((gemm_kernel<A_MN, B_KC, FA, FB, EPI_DIRECT, FUSE>), grid, block, 0, s, p);
+      break;
+  }
+  return hipGetLastError();
+}
+
+template <bool A_MN, bool B_KC, bool FUSE>
+hipError_t launch_formats(const GemmParams& p, int fa, int fb, int epi, hipStream_t s) {
+  if (fa == kE4M3 && fb == kE4M3) return launch_fmt<A_MN, B_KC, FUSE, kE4M3, kE4M3>(p, epi, s);
+  if (fa == kE4M3 && fb == kE5M2) return launch_fmt<A_MN, B_KC, FUSE, kE4M3, kE5M2>(p, epi, s);
+  if (fa == kE5M2 && fb == kE4M3) return launch_fmt<A_MN, B_KC, FUSE, kE5M2, kE4M3>(p, epi, s);
+  return launch_fmt<A_MN, B_KC, FUSE, kE5M2, kE5M2>(p, epi, s);
+}
 
 }  // namespace scalify

@@ -7,10 +7,17 @@ namespace scalify {
 
 // Workspace header, in 32-bit words at the start of every workspace:
 //   [0] amax as fp32 bits (atomic max target; zeroed by the prologue)
-//   [1] exponent sum of the input scales (snapshot taken by the prologue, so
-//       that an output scale aliasing an input scale cannot race)
-//   [2] delayed rescale: the shift of the direct cast, data' = acc * 2^-shift
+//   [1] e_w, the scale exponent of the pre-cast value w (the exponent sum of
+//       the input scales, or the scaled-add exponent with a residual):
+//       snapshot taken by the prologue, so that an output scale aliasing an
+//       input scale cannot race
+//   [2] delayed rescale: the shift of the direct cast, data' = w * 2^-shift
+//   [3] fused residual add: shift of acc into w's scale (e_a + e_b - e_w)
+//   [4] fused residual add: shift of the residual (q - e_w)
 constexpr size_t kHeaderBytes = 256;
+
+// Activation of the fused epilogue (values of scalify_activation).
+enum Act : int { ACT_NONE = 0, ACT_RELU = 1, ACT_GELU_TANH = 2, ACT_SILU = 3 };
 
 // What the GEMM writes: a pre-cast intermediate for the cast kernel that
 // follows (16-bit rounding-preserving encoding for FP8 outputs, the fp32
@@ -34,23 +41,46 @@ struct GemmParams {
   void* out;       // EPI_DIRECT: output codes [M][ldc] of format out_fmt
   int64_t ldc;
   int out_fmt;
+  // Fused epilogue (FUSE kernels only): residual codes [M][ldr] (ldr = 0:
+  // one row for every row) of format res_fmt or NULL, activation, and the
+  // optional export of the pre-cast value w [M][N].
+  const void* res;
+  int64_t ldr;
+  int res_fmt;
+  int act;
+  float* pre_out;
 };
 
+// fuse: launch the kernels with the fused residual add / activation / pre_out
+// epilogue (the plain kernels otherwise).
 hipError_t launch_gemm(const GemmParams& p, bool a_mn, bool b_kc, int fa, int fb, int epi,
-                       hipStream_t s);
+                       bool fuse, hipStream_t s);
 
 // Prologue: hdr[0] = 0, hdr[1] = exponent(s0) + exponent(s1) (NULL = scale 1).
 hipError_t launch_prologue(uint32_t* hdr, const float* s0, const float* s1, hipStream_t s);
 
-// Prologue of the delayed rescale: as launch_prologue, plus the output scale
-// from the statistic *amax_in of an earlier call (e_r = floor(log2 amax_in)
-// - target, 0 when amax_in is 0, Inf or NaN): writes *out_scale = 2^e_out,
-// e_out = clamp(e_a + e_b + e_c + e_r), and hdr[2] = e_out - e_a - e_b.
-hipError_t launch_prologue_delayed(uint32_t* hdr, const float* s0, const float* s1,
-                                   const float* amax_in, int e_c, int target, float* out_scale,
-                                   hipStream_t s);
+// Prologue of the matmul: hdr[0] = 0 and hdr[1] = e_w, the scale exponent of
+// the pre-cast value: e_a + e_b, or with a residual of scale 2^q the scaled
+// add exponent max(e_a + e_b + e_c, q) (sqrt(s_p^2 + s_r^2) rounded down),
+// with hdr[3] = e_a + e_b - e_w and hdr[4] = q - e_w. Delayed rescale: the
+// output scale from the statistic *amax_in of an earlier call (e_r =
+// floor(log2 amax_in) - target, 0 when amax_in is 0, Inf or NaN): writes
+// *out_scale = 2^e_out, e_out = clamp(e_w + e_cc + e_r), and hdr[2] =
+// e_out - e_w, where e_cc = e_c without a residual and 0 with one.
+struct MatmulPrologue {
+  const float* s0;
+  const float* s1;
+  const float* s_res;  // residual scale (NULL = 1)
+  int residual;        // 1: scaled add of a residual
+  int e_c;
+  int delayed;
+  const float* amax_in;
+  int target;
+  float* out_scale;
+};
+hipError_t launch_matmul_prologue(uint32_t* hdr, const MatmulPrologue& q, hipStream_t s);
 
-// *amax_out = amax recorded in hdr[0] (max |acc|) times 2^-e_c.
+// *amax_out = amax recorded in hdr[0] (max |w|) times 2^-e_cc.
 hipError_t launch_finalize_amax(const uint32_t* hdr, int e_c, float* amax_out, hipStream_t s);
 
 // Cast of the GEMM intermediate [M][ldw] to out [M][ldc]; computes the

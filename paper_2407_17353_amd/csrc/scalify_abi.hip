@@ -34,12 +34,40 @@ scalify_status check_matrix(const scalify_scaled_array* x, int64_t ld_multiple) 
   return SCALIFY_OK;
 }
 
-size_t matmul_ws(int64_t M, int64_t N, int32_t out_dtype, int32_t rescale) {
+// fused: the call fuses a residual add or an activation, or exports pre_out;
+// its intermediate is then fp32 (exact for every pre-cast value, fp32
+// subnormals included).
+size_t matmul_ws(int64_t M, int64_t N, int32_t out_dtype, int32_t rescale, bool fused) {
   if (M < 0 || N < 0 || !is_out(out_dtype) || rescale < SCALIFY_RESCALE_NONE ||
       rescale > SCALIFY_RESCALE_DELAYED)
     return 0;
   if (rescale == SCALIFY_RESCALE_DELAYED) return kHeaderBytes;  // codes written by the GEMM
-  return kHeaderBytes + (size_t)M * (size_t)round_up(N, 16) * (out_dtype == SCALIFY_F16 ? 4u : 2u);
+  const size_t bytes = (out_dtype == SCALIFY_F16 || fused) ? 4u : 2u;
+  return kHeaderBytes + (size_t)M * (size_t)round_up(N, 16) * bytes;
+}
+
+bool is_fused(const scalify_matmul_opts* o) {
+  return o->residual != nullptr || o->activation != SCALIFY_ACT_NONE || o->pre_out != nullptr;
+}
+
+// Residual of the fused scaled add: M x N, row-major, ld = 0 (one row for
+// every row) or ld >= N; the very same matrix as out, or disjoint from it.
+scalify_status check_residual(const scalify_scaled_array* r, const scalify_scaled_array* out,
+                              int64_t M, int64_t N) {
+  if (!is_out(r->dtype)) return SCALIFY_ERR_DTYPE;
+  if (r->rows != M || r->cols != N) return SCALIFY_ERR_SHAPE;
+  if (r->trans != 0) return SCALIFY_ERR_LAYOUT;
+  if (M == 0 || N == 0) return SCALIFY_OK;
+  if (r->data == nullptr) return SCALIFY_ERR_NULL;
+  if (r->ld != 0 && r->ld < N) return SCALIFY_ERR_SHAPE;
+  if (r->ld % (r->dtype == SCALIFY_F16 ? 8 : 16) != 0 || !aligned16(r->data)) return SCALIFY_ERR_ALIGN;
+  const uintptr_t r0 = (uintptr_t)r->data;
+  const uintptr_t r1 = r0 + (uintptr_t)(((r->ld ? (M - 1) * r->ld : 0) + N) * elem_bytes(r->dtype));
+  const uintptr_t o0 = (uintptr_t)out->data;
+  const uintptr_t o1 = o0 + (uintptr_t)(((M - 1) * out->ld + N) * elem_bytes(out->dtype));
+  const bool same = r->data == out->data && r->dtype == out->dtype && r->ld == out->ld;
+  if (r0 < o1 && o0 < r1 && !same) return SCALIFY_ERR_LAYOUT;
+  return SCALIFY_OK;
 }
 
 scalify_status check_elementwise(const scalify_scaled_array* in, const scalify_scaled_array* out) {
@@ -75,7 +103,12 @@ int32_t scalify_matmul_scale_log2(int64_t K) {
 }
 
 size_t scalify_matmul_workspace_size(int64_t M, int64_t N, int32_t out_dtype, int32_t rescale) {
-  return matmul_ws(M, N, out_dtype, rescale);
+  return matmul_ws(M, N, out_dtype, rescale, false);
+}
+
+size_t scalify_matmul_workspace_size_opts(int64_t M, int64_t N, const scalify_matmul_opts* opts) {
+  if (!opts) return 0;
+  return matmul_ws(M, N, opts->out_dtype, opts->rescale, is_fused(opts));
 }
 
 size_t scalify_rescale_workspace_size(int64_t n) { return n < 0 ? 0 : kHeaderBytes; }
@@ -107,6 +140,8 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
     return SCALIFY_ERR_VALUE;
   if (opts->rescale == SCALIFY_RESCALE_DELAYED && !opts->amax_in) return SCALIFY_ERR_NULL;
   if (opts->target_log2 < -1000 || opts->target_log2 > 1000) return SCALIFY_ERR_VALUE;
+  if (opts->activation < SCALIFY_ACT_NONE || opts->activation > SCALIFY_ACT_SILU)
+    return SCALIFY_ERR_VALUE;
   if (out->trans != 0) return SCALIFY_ERR_LAYOUT;
   const int64_t M = a->rows, K = a->cols, N = b->cols;
   if (b->rows != K || out->rows != M || out->cols != N) return SCALIFY_ERR_SHAPE;
@@ -114,11 +149,14 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
   if ((st = check_matrix(a, 16)) != SCALIFY_OK) return st;
   if ((st = check_matrix(b, 16)) != SCALIFY_OK) return st;
   if ((st = check_matrix(out, out->dtype == SCALIFY_F16 ? 8 : 16)) != SCALIFY_OK) return st;
+  const scalify_scaled_array* res = opts->residual;
+  if (res && (st = check_residual(res, out, M, N)) != SCALIFY_OK) return st;
+  const bool fused = is_fused(opts);
   // 32-bit byte offsets inside the GEMM kernel, including the range-checked
   // reads of up to one tile past the last stored row.
   if (M && K && (stored_rows(a) + 256) * a->ld + 256 >= ((int64_t)1 << 32)) return SCALIFY_ERR_SHAPE;
   if (K && N && (stored_rows(b) + 256) * b->ld + 256 >= ((int64_t)1 << 32)) return SCALIFY_ERR_SHAPE;
-  const size_t need = matmul_ws(M, N, opts->out_dtype, opts->rescale);
+  const size_t need = matmul_ws(M, N, opts->out_dtype, opts->rescale, fused);
   if (!workspace || workspace_bytes < need || ((uintptr_t)workspace & 255u))
     return SCALIFY_ERR_WORKSPACE;
 
@@ -127,17 +165,27 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
   const int e_c = scalify_matmul_scale_log2(K);
   const bool amax_mode = opts->rescale == SCALIFY_RESCALE_AMAX;
   const bool delayed = opts->rescale == SCALIFY_RESCALE_DELAYED;
-  const int epi = delayed ? EPI_DIRECT : (opts->out_dtype == SCALIFY_F16 ? EPI_INTER32 : EPI_INTER16);
+  // Delayed: the output scale comes from the statistic of an earlier call,
+  // so the GEMM casts straight to codes (no intermediate). Otherwise the GEMM
+  // writes a pre-cast intermediate: 16-bit for FP8 outputs of the plain
+  // epilogue, fp32 for FP16 outputs and for fused epilogues.
+  const int epi = delayed ? EPI_DIRECT
+                          : ((opts->out_dtype == SCALIFY_F16 || fused) ? EPI_INTER32 : EPI_INTER16);
+  // Exponent offset of the statistic: the matmul data is acc * 2^-e_c; with
+  // a residual the statistic is taken over w itself.
+  const int e_cc = res ? 0 : e_c;
 
-  if (delayed) {
-    // The output scale comes from the statistic of an earlier call, so the
-    // GEMM casts its accumulators straight to codes: no intermediate.
-    if (launch_prologue_delayed(hdr, a->scale, b->scale, opts->amax_in, e_c, opts->target_log2,
-                                out->scale, s) != hipSuccess)
-      return SCALIFY_ERR_HIP;
-  } else if (launch_prologue(hdr, a->scale, b->scale, s) != hipSuccess) {
-    return SCALIFY_ERR_HIP;
-  }
+  MatmulPrologue pq = {};
+  pq.s0 = a->scale;
+  pq.s1 = b->scale;
+  pq.s_res = res ? res->scale : nullptr;
+  pq.residual = res ? 1 : 0;
+  pq.e_c = e_c;
+  pq.delayed = delayed ? 1 : 0;
+  pq.amax_in = opts->amax_in;
+  pq.target = opts->target_log2;
+  pq.out_scale = out->scale;
+  if (launch_matmul_prologue(hdr, pq, s) != hipSuccess) return SCALIFY_ERR_HIP;
 
   GemmParams p = {};
   p.a = (const uint8_t*)a->data;
@@ -160,16 +208,22 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
   p.out = out->data;
   p.ldc = out->ld;
   p.out_fmt = opts->out_dtype;
+  p.res = res && M > 0 && N > 0 ? res->data : nullptr;
+  p.ldr = res ? res->ld : 0;
+  p.res_fmt = res ? res->dtype : 0;
+  p.act = opts->activation;
+  p.pre_out = opts->pre_out;
   hipEvent_t* ev = (hipEvent_t*)opts->events;
   if (ev && ev[0] && hipEventRecord(ev[0], s) != hipSuccess) return SCALIFY_ERR_HIP;
   if (M > 0 && N > 0) {
-    if (launch_gemm(p, a->trans != 0, b->trans != 0, a->dtype, b->dtype, epi, s) != hipSuccess)
+    if (launch_gemm(p, a->trans != 0, b->trans != 0, a->dtype, b->dtype, epi, fused, s) !=
+        hipSuccess)
       return SCALIFY_ERR_HIP;
   }
   if (ev && ev[1] && hipEventRecord(ev[1], s) != hipSuccess) return SCALIFY_ERR_HIP;
   if (delayed) {
     // The statistic this call records for the next one.
-    if (opts->amax_out && launch_finalize_amax(hdr, e_c, opts->amax_out, s) != hipSuccess)
+    if (opts->amax_out && launch_finalize_amax(hdr, e_cc, opts->amax_out, s) != hipSuccess)
       return SCALIFY_ERR_HIP;
   } else {
     // Second pass: global amax -> rescale exponent -> output scale, and the
@@ -181,7 +235,7 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
     q.ldc = out->ld;
     q.M = N > 0 ? (int)M : 0;
     q.N = (int)N;
-    q.e_c = e_c;
+    q.e_c = e_cc;
     q.target = opts->target_log2;
     q.sat = p.sat;
     q.mode = amax_mode ? 1 : 0;

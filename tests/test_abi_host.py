@@ -158,3 +158,67 @@ def test_rescale_and_set_scaling_specific_errors():
     assert lib.scalify_set_scaling(ctypes.byref(x), ctypes.byref(y), 128, 1, None) == 7
     y2 = arr(4, 64, ld=64, data=FAKE + 65536, scale=x.scale)
     assert lib.scalify_set_scaling(ctypes.byref(x), ctypes.byref(y2), 3, 1, None) == 4
+
+
+def test_fused_workspace_sizes():
+    """A fused residual add / activation / pre_out keeps an fp32 intermediate."""
+    assert sc.scalify_matmul_workspace_size_opts(8192, 8192, sc.E4M3) == 256 + 8192 * 8192 * 2
+    assert sc.scalify_matmul_workspace_size_opts(8192, 8192, sc.E4M3, fused=True) == \
+        256 + 8192 * 8192 * 4
+    assert sc.scalify_matmul_workspace_size_opts(17, 33, sc.E5M2, fused=True) == 256 + 17 * 48 * 4
+    assert sc.scalify_matmul_workspace_size_opts(10, 10, sc.F16, fused=True) == 256 + 10 * 16 * 4
+    assert sc.scalify_matmul_workspace_size_opts(10, 10, sc.E4M3, sc.RESCALE_DELAYED, True) == 256
+    assert sc.load_library().scalify_matmul_workspace_size_opts(10, 10, None) == 0
+
+
+def fused_opts(residual=None, act=sc.ACT_NONE, pre_out=None, out_dtype=sc.E4M3,
+               mode=sc.RESCALE_AMAX):
+    o = sc.CMatmulOpts(out_dtype, mode, 0, 1, None, None, None, None, None, act, pre_out)
+    if residual is not None:
+        o.residual = ctypes.pointer(residual)
+    return o
+
+
+@pytest.mark.parametrize("case,status", [
+    ("act_high", 7), ("act_negative", 7), ("res_f32", 2), ("res_rows", 3), ("res_cols", 3),
+    ("res_trans", 4), ("res_ld_small", 3), ("res_ld_unaligned", 5), ("res_f16_ld", 5),
+    ("res_ptr_unaligned", 5), ("res_null_data", 1), ("res_overlaps_out", 4),
+    ("res_same_data_other_ld", 4), ("res_broadcast_over_out", 4), ("ws_too_small_for_fused", 6),
+])
+def test_matmul_fused_argument_errors(case, status):
+    a, b, out = arr(64, 128), arr(128, 32), arr(64, 32, data=FAKE + (1 << 20))
+    res = arr(64, 32, data=FAKE + (2 << 20))
+    kw = {}
+    opts = None
+    if case == "act_high":
+        opts = fused_opts(act=4)
+    elif case == "act_negative":
+        opts = fused_opts(act=-1)
+    elif case == "res_f32":
+        opts = fused_opts(arr(64, 32, dtype=sc.F32, data=FAKE + (2 << 20)))
+    elif case == "res_rows":
+        opts = fused_opts(arr(63, 32, data=FAKE + (2 << 20)))
+    elif case == "res_cols":
+        opts = fused_opts(arr(64, 48, data=FAKE + (2 << 20)))
+    elif case == "res_trans":
+        opts = fused_opts(arr(64, 32, trans=1, data=FAKE + (2 << 20)))
+    elif case == "res_ld_small":
+        opts = fused_opts(arr(64, 32, ld=16, data=FAKE + (2 << 20)))
+    elif case == "res_ld_unaligned":
+        opts = fused_opts(arr(64, 32, ld=40, data=FAKE + (2 << 20)))
+    elif case == "res_f16_ld":
+        opts = fused_opts(arr(64, 32, dtype=sc.F16, ld=36, data=FAKE + (2 << 20)))
+    elif case == "res_ptr_unaligned":
+        opts = fused_opts(arr(64, 32, data=FAKE + (2 << 20) + 4))
+    elif case == "res_null_data":
+        opts = fused_opts(arr(64, 32, data=None))
+    elif case == "res_overlaps_out":
+        opts = fused_opts(arr(64, 32, data=FAKE + (1 << 20) + 64))
+    elif case == "res_same_data_other_ld":
+        opts = fused_opts(arr(64, 32, ld=48, data=FAKE + (1 << 20)))
+    elif case == "res_broadcast_over_out":
+        opts = fused_opts(arr(64, 32, ld=0, data=FAKE + (1 << 20)))
+    elif case == "ws_too_small_for_fused":
+        opts = fused_opts(res)
+        kw["ws_bytes"] = sc.scalify_matmul_workspace_size(64, 32, sc.E4M3)
+    assert call_matmul(a, b, out, opts=opts, **kw) == status
