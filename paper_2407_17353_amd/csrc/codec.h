@@ -120,6 +120,13 @@ typedef short v2s_t __attribute__((ext_vector_type(2)));
 // Largest |shift| for which 2^shift is a normal fp32.
 constexpr int kFastShiftMax = 126;
 
+// Smallest shift for the fast paths when inputs may be fp32 subnormals: with
+// shift >= kFastShiftMinSub a subnormal x (|x| < 2^-126) scales to less than
+// 2^-26, under half the smallest FP16 (and FP8) subnormal, so its code is a
+// zero of its sign whether or not the conversion flushes subnormal inputs
+// (the sign is kept either way). Below it such inputs need the exact cast.
+constexpr int kFastShiftMinSub = -100;
+
 // Saturation fix-up on 4 packed codes: overflow codes -> +-max (same sign).
 // E4M3 overflow is 0x7F|s (max 0x7E|s); E5M2 overflow is 0x7C|s (0x7B|s):
 // subtract one in exactly the bytes whose low 7 bits equal the overflow code.
@@ -153,13 +160,6 @@ __device__ __forceinline__ uint32_t cast4_fp8_hw(uint32_t u0, uint32_t u1, uint3
 }
 
 __device__ __forceinline__ bool is_nan_bits(uint32_t u) { return (u & 0x7FFFFFFFu) > 0x7F800000u; }
-
-// NaN, or a nonzero fp32 subnormal: inputs that take the exact integer cast
-// instead of the hardware conversions.
-__device__ __forceinline__ bool needs_exact_bits(uint32_t u) {
-  const uint32_t e = u & 0x7F800000u;
-  return (e == 0x7F800000u || e == 0u) && (u & 0x7FFFFFu) != 0u;
-}
 
 // Exact fp32 bits of an FP8 / FP16 code (all FP8 and FP16 values are fp32).
 template <int F>

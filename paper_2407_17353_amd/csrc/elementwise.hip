@@ -138,15 +138,15 @@ __device__ __forceinline__ void store1(void* base, int64_t e, uint32_t c) {
 
 // 16 fp32 values (bits) times 2^-shift -> 16 codes packed in 4 words (FP8)
 // or 8 words (FP16: two codes per word). FP8 uses the hardware conversion
-// when the scale fits and no value is NaN or an fp32 subnormal, else the
-// integer cast.
+// when `fast` (the shift is in the window where it is exact, fp32
+// subnormal inputs included) and no value is NaN, else the integer cast.
 template <int OUTF>
 __device__ __forceinline__ void encode16(const uint32_t (&u)[16], int shift, float scale, bool fast,
                                          bool sat, uint32_t (&w)[8]) {
   if (OUTF == kE4M3 || OUTF == kE5M2) {
     bool nan = false;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) nan |= needs_exact_bits(u[i]);
+    for (int i = 0; i < 16; ++i) nan |= is_nan_bits(u[i]);
     if (fast && !nan) {
 #pragma unroll
       for (int q = 0; q < 4; ++q)
@@ -195,7 +195,7 @@ __global__ __launch_bounds__(EW_THREADS) void epilogue_cast_kernel(EpilogueParam
   const int e_out = clamp_e8m0(e_ab + p.e_c + e_r);
   const int shift = e_out - e_ab;  // data' = acc * 2^-shift
   const bool sat = p.sat != 0;
-  const bool fast = shift >= -kFastShiftMax && shift <= kFastShiftMax;
+  const bool fast = shift >= kFastShiftMinSub && shift <= kFastShiftMax;
   const float scale = fast ? pow2_float(shift) : 1.0f;
   if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) {
     *p.out_scale = pow2_float(e_out);
@@ -305,7 +305,7 @@ __global__ __launch_bounds__(EW_THREADS) void elementwise_kernel(ElemParams p) {
     shift = e_out - e_in;
   }
   const bool sat = p.sat != 0;
-  const bool fast = shift >= -kFastShiftMax && shift <= kFastShiftMax;
+  const bool fast = shift >= kFastShiftMinSub && shift <= kFastShiftMax;
   const float scale = fast ? pow2_float(shift) : 1.0f;
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     if (p.rule == RULE_COPY) *p.out_scale = p.in_scale ? *p.in_scale : 1.0f;

@@ -219,8 +219,8 @@ __device__ __forceinline__ void static_for(F&& f) {
 
 // Direct cast of 4 pre-cast values (fp32 bits) times 2^-shift, for the
 // delayed rescale. Fast paths use the hardware conversions (callers check
-// that |shift| <= kFastShiftMax and that no value is NaN, nor, in the fused
-// kernels, an fp32 subnormal); the exact integer casts are kept out of line.
+// that the shift is in their exact window and that no value is NaN); the
+// exact integer casts are kept out of line.
 __device__ __forceinline__ v2i cast4_f16_hw(uint32_t u0, uint32_t u1, uint32_t u2, uint32_t u3,
                                            float inv, bool sat) {
   // x * 2^-shift (inv = 2^-shift) is exact in fp32 unless it leaves the
@@ -290,61 +290,100 @@ __device__ __forceinline__ void load_residual_codes(const GemmParams& p, int m, 
   }
 }
 
-// Residual codes decoded exactly to fp32.
-__device__ __forceinline__ v4f decode_residual4(int fmt, const uint32_t (&c)[2]) {
+// Residual codes decoded to fp32 (exact: every FP8 and FP16 value is an
+// fp32) by the hardware conversions, OCP FP8 with a unit scale.
+__device__ __forceinline__ v4f decode_residual4(int fmt, uint32_t c0, uint32_t c1) {
   v4f r;
   if (fmt == kF16) {
-    r[0] = __uint_as_float(decode_bits<kF16>(c[0] & 0xFFFFu));
-    r[1] = __uint_as_float(decode_bits<kF16>(c[0] >> 16));
-    r[2] = __uint_as_float(decode_bits<kF16>(c[1] & 0xFFFFu));
-    r[3] = __uint_as_float(decode_bits<kF16>(c[1] >> 16));
+    r[0] = (float)__builtin_bit_cast(_Float16, (uint16_t)(c0 & 0xFFFFu));
+    r[1] = (float)__builtin_bit_cast(_Float16, (uint16_t)(c0 >> 16));
+    r[2] = (float)__builtin_bit_cast(_Float16, (uint16_t)(c1 & 0xFFFFu));
+    r[3] = (float)__builtin_bit_cast(_Float16, (uint16_t)(c1 >> 16));
   } else if (fmt == kE4M3) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) r[i] = __uint_as_float(decode_bits<kE4M3>((c[0] >> (8 * i)) & 0xFFu));
+    r[0] = __builtin_amdgcn_cvt_scalef32_f32_fp8(c0, 1.0f, 0);
+    r[1] = __builtin_amdgcn_cvt_scalef32_f32_fp8(c0, 1.0f, 1);
+    r[2] = __builtin_amdgcn_cvt_scalef32_f32_fp8(c0, 1.0f, 2);
+    r[3] = __builtin_amdgcn_cvt_scalef32_f32_fp8(c0, 1.0f, 3);
   } else {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) r[i] = __uint_as_float(decode_bits<kE5M2>((c[0] >> (8 * i)) & 0xFFu));
+    r[0] = __builtin_amdgcn_cvt_scalef32_f32_bf8(c0, 1.0f, 0);
+    r[1] = __builtin_amdgcn_cvt_scalef32_f32_bf8(c0, 1.0f, 1);
+    r[2] = __builtin_amdgcn_cvt_scalef32_f32_bf8(c0, 1.0f, 2);
+    r[3] = __builtin_amdgcn_cvt_scalef32_f32_bf8(c0, 1.0f, 3);
   }
   return r;
 }
 
 // Smooth gates in fp32: silu g(x) = 1 / (1 + e^-x); the tanh form of gelu
 // (1 + tanh(u)) / 2 with u = sqrt(2/pi) (x + 0.044715 x^3) is the same
-// sigmoid at 2u. Defined at +-Inf (1 and 0); NaN stays NaN. Within a few ulp
-// of the exact gate where it is a normal fp32 (below 2^-126 it may flush).
-__device__ __forceinline__ float smooth_gate(int act, float x) {
-  float t = x;
-  if (act == ACT_GELU_TANH) {
-    const float k0 = 1.5957691216057308f;   // 2 sqrt(2/pi)
-    const float k1 = 0.07135481627260025f;  // 2 sqrt(2/pi) * 0.044715
-    t = x * (k0 + k1 * (x * x));
-  }
+// sigmoid at 2u. Both are 1 and 0 at +-Inf and NaN for NaN, within a few
+// ulp of the exact gate where it is a normal fp32 (below 2^-126 it may
+// flush to 0).
+template <bool GELU>
+__device__ __forceinline__ float smooth_gate(float x) {
+  const float k0 = 1.5957691216057308f;   // 2 sqrt(2/pi)
+  const float k1 = 0.07135481627260025f;  // 2 sqrt(2/pi) * 0.044715
+  const float t = GELU ? x * (k0 + k1 * (x * x)) : x;
   return __builtin_amdgcn_rcpf(1.0f + expf(-t));
 }
 
-// w for 4 adjacent outputs: acc -> (scaled add of the residual codes rc0,
-// rc1 of format res_fmt when has_res) -> (activation act). sh_acc, sh_res:
-// power-of-two shifts of acc and of the residual into w's scale 2^e_w; the
-// gate sees the true value w * 2^e_w. Out of line: the epilogue calls it
-// once per 4 outputs, and one copy keeps the kernel's code small enough for
-// the instruction cache.
-__device__ __attribute__((noinline)) v4f fuse4(v4f v, uint32_t rc0, uint32_t rc1, int has_res,
-                                               int res_fmt, int act, int sh_acc, int sh_res,
-                                               int e_w) {
-  if (has_res) {
-    const uint32_t rc[2] = {rc0, rc1};
-    const v4f r = decode_residual4(res_fmt, rc);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) v[i] = ldexpf(v[i], sh_acc) + ldexpf(r[i], sh_res);
+// The fused pre-cast values of a wave's accumulators, in place: the scaled
+// add of the residual (format RF; power-of-two shifts sh_acc and sh_res into
+// w's scale 2^e_w), then the activation ACT, whose gate sees the true value
+// w * 2^e_w. One straight pass per transformation. The residual codes of all
+// the wave's outputs are loaded first, so that their latencies overlap; a
+// wave tile inside the matrix loads them without per-output checks.
+template <int RF, int MI_, int NI_>
+__device__ __forceinline__ void add_residual(const GemmParams& p, v4f (&acc)[MI_][NI_], int mb,
+                                             int nb, bool interior, int sh_acc, int sh_res) {
+  constexpr int W = RF == kF16 ? 2 : 1;  // code words per 4 outputs
+  uint32_t rc[MI_][NI_][W];
+  if (interior) {
+    static_for<0, MI_ * NI_>([&](auto I) {
+      constexpr int mi = decltype(I)::value / NI_, ni = decltype(I)::value % NI_;
+      const int64_t e = (int64_t)(mb + 16 * mi) * p.ldr + nb + 16 * ni;
+      if constexpr (RF == kF16) {
+        const v2i w = *(const v2i*)((const uint16_t*)p.res + e);
+        rc[mi][ni][0] = (uint32_t)w.x;
+        rc[mi][ni][W - 1] = (uint32_t)w.y;
+      } else {
+        rc[mi][ni][0] = *(const uint32_t*)((const uint8_t*)p.res + e);
+      }
+    });
+  } else {
+    static_for<0, MI_ * NI_>([&](auto I) {
+      constexpr int mi = decltype(I)::value / NI_, ni = decltype(I)::value % NI_;
+      const int m = mb + 16 * mi;
+      const int n = nb + 16 * ni;
+      uint32_t c[2] = {0u, 0u};
+      if (m < p.M && n < p.N) load_residual_codes(p, m, n, c);
+      rc[mi][ni][0] = c[0];
+      rc[mi][ni][W - 1] = RF == kF16 ? c[1] : c[0];
+    });
   }
-  if (act == ACT_RELU) {
+  static_for<0, MI_ * NI_>([&](auto I) {
+    constexpr int mi = decltype(I)::value / NI_, ni = decltype(I)::value % NI_;
+    const v4f r = decode_residual4(RF, rc[mi][ni][0], rc[mi][ni][W - 1]);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) v[i] = v[i] * (v[i] > 0.0f ? 1.0f : 0.0f);
-  } else if (act != ACT_NONE) {
+    for (int i = 0; i < 4; ++i) acc[mi][ni][i] = ldexpf(acc[mi][ni][i], sh_acc) + ldexpf(r[i], sh_res);
+    __builtin_amdgcn_sched_barrier(0);  // one group at a time: bounded register use
+  });
+}
+
+template <int ACT, int MI_, int NI_>
+__device__ __forceinline__ void activate(v4f (&acc)[MI_][NI_], int e_w) {
+  static_for<0, MI_ * NI_>([&](auto I) {
+    constexpr int mi = decltype(I)::value / NI_, ni = decltype(I)::value % NI_;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) v[i] = v[i] * smooth_gate(act, ldexpf(v[i], e_w));
-  }
-  return v;
+    for (int i = 0; i < 4; ++i) {
+      const float v = acc[mi][ni][i];
+      if constexpr (ACT == ACT_RELU) {
+        acc[mi][ni][i] = v * (v > 0.0f ? 1.0f : 0.0f);
+      } else {
+        acc[mi][ni][i] = v * smooth_gate<ACT == ACT_GELU_TANH>(ldexpf(v, e_w));
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);  // one group at a time: bounded register use
+  });
 }
 
 template <bool A_MN, bool B_KC, int FA, int FB, int EPI, bool FUSE>
@@ -503,38 +542,50 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
   const int nb = n0 + wn + 4 * (lane >> 4);
   // EPI_DIRECT: data' = acc * 2^-shift, shift from the prologue
   const int shift = EPI == EPI_DIRECT ? (int)__builtin_amdgcn_readfirstlane(p.hdr[2]) : 0;
-  const bool fast = shift >= -kFastShiftMax && shift <= kFastShiftMax;
+  // Fused values may be fp32 subnormals (the accumulators never are).
+  const bool fast = shift >= (FUSE ? kFastShiftMinSub : -kFastShiftMax) && shift <= kFastShiftMax;
   const float hw_scale = fast ? pow2_float(shift) : 1.0f;
   const float hw_inv = fast ? pow2_float(-shift) : 1.0f;
   const bool sat = p.sat != 0;
-  // FUSE: the shifts of the scaled add and the scale exponent of w.
-  int f_sh_acc = 0, f_sh_res = 0, f_ew = 0;
-  // FUSE: the residual codes of all the wave's outputs, loaded up front so
-  // that their memory latencies overlap.
-  uint32_t rcodes[FUSE ? MI : 1][FUSE ? NI : 1][2] = {};
+  // FUSE: a first pass turns every accumulator into its pre-cast value w
+  // (scaled add, activation) before any store is issued, so that the only
+  // memory waits are those of the residual codes, all loaded up front; the
+  // pass below then writes w as the plain epilogue writes acc.
   if constexpr (FUSE) {
-    f_ew = (int)__builtin_amdgcn_readfirstlane(p.hdr[1]);
-    if (p.res) {
-      f_sh_acc = (int)__builtin_amdgcn_readfirstlane(p.hdr[3]);
-      f_sh_res = (int)__builtin_amdgcn_readfirstlane(p.hdr[4]);
+    const int e_w = (int)__builtin_amdgcn_readfirstlane(p.hdr[1]);
+    if (p.acc_out) {
       static_for<0, MI * NI>([&](auto I) {
         constexpr int mi = decltype(I)::value / NI, ni = decltype(I)::value % NI;
         const int m = mb + 16 * mi;
         const int n = nb + 16 * ni;
-        if (m < M && n < N) load_residual_codes(p, m, n, rcodes[mi][ni]);
+        if (m < M && n < N) {
+          const v4f a = acc[mi][ni];
+          float* q = p.acc_out + (int64_t)m * N + n;
+          q[0] = a[0];
+          if (n + 1 < N) q[1] = a[1];
+          if (n + 2 < N) q[2] = a[2];
+          if (n + 3 < N) q[3] = a[3];
+        }
       });
     }
+    if (p.res) {
+      const bool interior = m0 + wm + 16 * MI <= M && n0 + wn + 16 * NI <= N;
+      const int sh_acc = (int)__builtin_amdgcn_readfirstlane(p.hdr[3]);
+      const int sh_res = (int)__builtin_amdgcn_readfirstlane(p.hdr[4]);
+      if (p.res_fmt == kE4M3) add_residual<kE4M3>(p, acc, mb, nb, interior, sh_acc, sh_res);
+      else if (p.res_fmt == kE5M2) add_residual<kE5M2>(p, acc, mb, nb, interior, sh_acc, sh_res);
+      else add_residual<kF16>(p, acc, mb, nb, interior, sh_acc, sh_res);
+    }
+    if (p.act == ACT_RELU) activate<ACT_RELU>(acc, e_w);
+    else if (p.act == ACT_GELU_TANH) activate<ACT_GELU_TANH>(acc, e_w);
+    else if (p.act == ACT_SILU) activate<ACT_SILU>(acc, e_w);
   }
   static_for<0, MI * NI>([&](auto I) {
     constexpr int mi = decltype(I)::value / NI, ni = decltype(I)::value % NI;
     const int m = mb + 16 * mi;
     const int n = nb + 16 * ni;
     if (m < M && n < N) {
-      v4f v = acc[mi][ni];
-      if constexpr (FUSE) {
-        const uint32_t(&rc)[2] = rcodes[FUSE ? mi : 0][FUSE ? ni : 0];
-        v = fuse4(v, rc[0], rc[1], p.res != nullptr, p.res_fmt, p.act, f_sh_acc, f_sh_res, f_ew);
-      }
+      const v4f v = acc[mi][ni];  // FUSE: w
       lmax = fmaxf(lmax, fabsf(v[0]));
       if (n + 1 < N) lmax = fmaxf(lmax, fabsf(v[1]));
       if (n + 2 < N) lmax = fmaxf(lmax, fabsf(v[2]));
@@ -553,10 +604,7 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
         // Hardware conversions unless a lane of the wave holds a NaN or the
         // shift is out of their range (then the exact integer cast, out of
         // line: it is rare and large).
-        const bool nan = FUSE ? (needs_exact_bits(u0) || needs_exact_bits(u1) ||
-                                 needs_exact_bits(u2) || needs_exact_bits(u3))
-                              : (is_nan_bits(u0) || is_nan_bits(u1) || is_nan_bits(u2) ||
-                                 is_nan_bits(u3));
+        const bool nan = is_nan_bits(u0) || is_nan_bits(u1) || is_nan_bits(u2) || is_nan_bits(u3);
         const bool hw = fast && !__any(nan);
         if (p.out_fmt == kF16) {
           v2i w;
@@ -591,7 +639,7 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
           }
         }
       }
-      if (p.acc_out) {
+      if (!FUSE && p.acc_out) {
         const v4f a = acc[mi][ni];
         float* q = p.acc_out + (int64_t)m * N + n;
         q[0] = a[0];
