@@ -15,6 +15,8 @@ Every function states the passage of the paper it follows:
     (Appendix A).
   * scaled add (Algorithm 3: sqrt of the sum of squared scales, rounded down)
     and activations f(x) = x * g(x) with the scale unchanged (Appendix C.1).
+  * LayerNorm on the data component with output scale 1 (Appendix C.2) and
+    its input gradient with a dynamic rescale (Section 4).
 
 Parity pins for every function live in tests/test_oracle_pins.py.
 """
@@ -92,6 +94,8 @@ def _load():
     lib.or_finish_pre.argtypes = [vp, c_i64, c_i32, c_i32, c_int, c_i32, c_f32, c_int, c_int, vp,
                                   ctypes.POINTER(c_f32)]
     lib.or_finish_pre.restype = c_i32
+    lib.or_layernorm_fwd_pre.argtypes = [c_int, vp, c_i64, c_i64, vp, vp, c_f64, vp, vp, vp]
+    lib.or_layernorm_bwd_pre.argtypes = [c_int, vp, c_int, vp, c_i64, c_i64, vp, c_f64, vp, vp, vp]
     lib.or_init()
     _lib = lib
     return lib
@@ -300,6 +304,73 @@ def matmul_epilogue_fused(acc, s_a, s_b, K, residual=None, act=ACT_NONE, mode=RE
     w, y64, e_w, e_cc = fused_pre(acc, s_a, s_b, K, residual, act)
     codes, e_out, amax = finish_pre(w, e_w, e_cc, mode, target_log2, amax_in, saturate, out_fmt)
     return codes, e_out, amax, w, y64
+
+
+# --------------------------------------------------------------------------- LayerNorm
+
+def _f32_or_none(a):
+    return None if a is None else np.ascontiguousarray(a, dtype=np.float32)
+
+
+def layernorm_fwd_pre(x, in_fmt: int, gamma=None, beta=None, eps: float = 1e-5):
+    """Scaled LayerNorm forward on the data component (Appendix C.2): per row,
+    xhat = (x - mean) / (std + eps), y = xhat * gamma + beta, output scale 1.
+    x: codes (or fp32 values for F32) [R, D]. Returns (y64, mean, std), fp64."""
+    lib = _load()
+    x = np.ascontiguousarray(x, dtype=_code_dtype(in_fmt))
+    R, D = x.shape
+    y = np.empty((R, D), dtype=np.float64)
+    mu = np.empty(R, dtype=np.float64)
+    sd = np.empty(R, dtype=np.float64)
+    g, b = _f32_or_none(gamma), _f32_or_none(beta)
+    lib.or_layernorm_fwd_pre(int(in_fmt), _ptr(x), R, D, _ptr(g) if g is not None else None,
+                             _ptr(b) if b is not None else None, float(eps), _ptr(y), _ptr(mu),
+                             _ptr(sd))
+    return y, mu, sd
+
+
+def layernorm_fwd(x, in_fmt: int, gamma=None, beta=None, eps: float = 1e-5, saturate: bool = True,
+                  out_fmt: int = E4M3):
+    """Forward with the output cast: y rounded to fp32, then to out_fmt with
+    scale 1 (Appendix C.2). Returns (codes, y64, mean, std)."""
+    y64, mu, sd = layernorm_fwd_pre(x, in_fmt, gamma, beta, eps)
+    codes, e_out, _ = finish_pre(y64.astype(np.float32), 0, 0, RESCALE_NONE, 0, 0.0, saturate,
+                                 out_fmt)
+    assert e_out == 0
+    return codes, y64, mu, sd
+
+
+def layernorm_bwd_pre(dy, dy_fmt: int, x, x_fmt: int, gamma=None, eps: float = 1e-5):
+    """Gradient of the data-component LayerNorm (Appendix C.2) for an
+    upstream gradient with data dy: returns (dx64, dgamma, dbeta) in fp64;
+    the true input gradient is dx64 * s_dy / X_s, the parameter gradients
+    are in units of s_dy."""
+    lib = _load()
+    dy = np.ascontiguousarray(dy, dtype=_code_dtype(dy_fmt))
+    x = np.ascontiguousarray(x, dtype=_code_dtype(x_fmt))
+    assert dy.shape == x.shape
+    R, D = x.shape
+    dx = np.empty((R, D), dtype=np.float64)
+    dg = np.empty(D, dtype=np.float64)
+    db = np.empty(D, dtype=np.float64)
+    g = _f32_or_none(gamma)
+    lib.or_layernorm_bwd_pre(int(dy_fmt), _ptr(dy), int(x_fmt), _ptr(x), R, D,
+                             _ptr(g) if g is not None else None, float(eps), _ptr(dx), _ptr(dg),
+                             _ptr(db))
+    return dx, dg, db
+
+
+def layernorm_bwd(dy, dy_fmt, s_dy, x, x_fmt, s_x, gamma=None, eps=1e-5, mode=RESCALE_AMAX,
+                  target_log2=0, saturate=True, out_fmt=E5M2):
+    """LayerNorm input gradient with its dynamic rescale (Section 4, the
+    LayerNorm backward rescale; Section 3.3): the ScaledArray (dx, s_dy / s_x)
+    rebalanced by the amax rule and cast. Returns (codes, e_out, amax, dx64,
+    dgamma, dbeta)."""
+    dx64, dg, db = layernorm_bwd_pre(dy, dy_fmt, x, x_fmt, gamma, eps)
+    e_in = int(_load().or_floor_log2(float(s_dy))) - int(_load().or_floor_log2(float(s_x)))
+    codes, e_out, amax = finish_pre(dx64.astype(np.float32), e_in, 0, mode, target_log2, 0.0,
+                                    saturate, out_fmt)
+    return codes, e_out, amax, dx64, dg, db
 
 
 # --------------------------------------------------------------------------- rescale / cast

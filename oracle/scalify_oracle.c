@@ -635,3 +635,106 @@ int32_t or_finish_pre(const float* w, int64_t n, int32_t e_w, int32_t e_cc, int 
     }
     return e_out;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Scaled LayerNorm (Appendix C.2; the custom LayerNorm of the experiments,  */
+/* with the dynamic rescale of its input gradient, Section 4).               */
+/* ------------------------------------------------------------------------ */
+
+/* Forward on the data component, one row of D values x (true value x * X_s):
+ * the normalization is scale invariant up to eps, so it normalizes X_d and
+ * gives the output scale 1:
+ *   mu = mean(x), sigma = sqrt(mean((x - mu)^2)), xhat = (x - mu) / (sigma + eps),
+ *   y = xhat * gamma + beta   (gamma NULL = 1, beta NULL = 0).
+ * fp64 throughout; y64 (optional) gets y, mu_out / sigma_out (optional) the
+ * row statistics. Rows are independent. */
+void or_layernorm_fwd_pre(int in_fmt, const void* x, int64_t R, int64_t D, const float* gamma,
+                          const float* beta, double eps, double* y64, double* mu_out,
+                          double* sigma_out)
+{
+    int64_t r;
+    double* v = (double*)malloc(sizeof(double) * (size_t)(D > 0 ? D : 1));
+    for (r = 0; r < R; ++r) {
+        double mu = 0.0, var = 0.0, sigma, den;
+        int64_t j;
+        for (j = 0; j < D; ++j) {
+            int64_t k = r * D + j;
+            if (in_fmt == OR_F32) v[j] = (double)((const float*)x)[k];
+            else if (in_fmt == OR_F16) v[j] = or_decode(OR_F16, ((const uint16_t*)x)[k]);
+            else v[j] = or_decode(in_fmt, ((const uint8_t*)x)[k]);
+            mu += v[j];
+        }
+        mu /= (double)D;
+        for (j = 0; j < D; ++j) var += (v[j] - mu) * (v[j] - mu);
+        var /= (double)D;
+        sigma = sqrt(var);
+        den = sigma + eps;
+        for (j = 0; j < D; ++j) {
+            double xh = (v[j] - mu) / den;
+            double y = xh * (gamma ? (double)gamma[j] : 1.0) + (beta ? (double)beta[j] : 0.0);
+            if (y64) y64[r * D + j] = y;
+        }
+        if (mu_out) mu_out[r] = mu;
+        if (sigma_out) sigma_out[r] = sigma;
+    }
+    free(v);
+}
+
+/* Backward of the forward above with respect to the data component, for an
+ * upstream gradient whose true value is dy * s_dy. With c = x - mu,
+ * s = sigma + eps, xhat = c / s and g = dy * gamma:
+ *   dL/dx_d = (1/s) (g - mean(g) - (c / sigma) mean(g * xhat)) * s_dy
+ * (the last term is 0 for a constant row, sigma = 0, where its limit is 0
+ * for eps > 0). As x = X_d * X_s, dL/dX = dL/dx_d / X_s: the gradient is the
+ * ScaledArray (dx, s_dy / X_s) with
+ *   dx = (1/s) (g - mean(g) - (c / sigma) mean(g * xhat)),
+ * which the dynamic rescale then rebalances (Section 4: the rescale of the
+ * LayerNorm input gradient). Also the parameter gradients, in units of s_dy:
+ *   dgamma_j = sum_r dy[r,j] * xhat[r,j],   dbeta_j = sum_r dy[r,j].
+ * fp64 throughout; every output is optional. */
+void or_layernorm_bwd_pre(int dy_fmt, const void* dy, int x_fmt, const void* x, int64_t R,
+                          int64_t D, const float* gamma, double eps, double* dx64,
+                          double* dgamma, double* dbeta)
+{
+    int64_t r, j;
+    double* v = (double*)malloc(sizeof(double) * (size_t)(D > 0 ? D : 1));
+    double* g = (double*)malloc(sizeof(double) * (size_t)(D > 0 ? D : 1));
+    double* d = (double*)malloc(sizeof(double) * (size_t)(D > 0 ? D : 1));
+    if (dgamma) for (j = 0; j < D; ++j) dgamma[j] = 0.0;
+    if (dbeta) for (j = 0; j < D; ++j) dbeta[j] = 0.0;
+    for (r = 0; r < R; ++r) {
+        double mu = 0.0, var = 0.0, sigma, s, mg = 0.0, mgx = 0.0;
+        for (j = 0; j < D; ++j) {
+            int64_t k = r * D + j;
+            if (x_fmt == OR_F32) v[j] = (double)((const float*)x)[k];
+            else if (x_fmt == OR_F16) v[j] = or_decode(OR_F16, ((const uint16_t*)x)[k]);
+            else v[j] = or_decode(x_fmt, ((const uint8_t*)x)[k]);
+            if (dy_fmt == OR_F32) d[j] = (double)((const float*)dy)[k];
+            else if (dy_fmt == OR_F16) d[j] = or_decode(OR_F16, ((const uint16_t*)dy)[k]);
+            else d[j] = or_decode(dy_fmt, ((const uint8_t*)dy)[k]);
+            mu += v[j];
+        }
+        mu /= (double)D;
+        for (j = 0; j < D; ++j) var += (v[j] - mu) * (v[j] - mu);
+        var /= (double)D;
+        sigma = sqrt(var);
+        s = sigma + eps;
+        for (j = 0; j < D; ++j) {
+            double xh = (v[j] - mu) / s;
+            g[j] = d[j] * (gamma ? (double)gamma[j] : 1.0);
+            mg += g[j];
+            mgx += g[j] * xh;
+            if (dgamma) dgamma[j] += d[j] * xh;
+            if (dbeta) dbeta[j] += d[j];
+        }
+        mg /= (double)D;
+        mgx /= (double)D;
+        for (j = 0; j < D; ++j) {
+            double t = sigma > 0.0 ? ((v[j] - mu) / sigma) * mgx : 0.0;
+            if (dx64) dx64[r * D + j] = (g[j] - mg - t) / s;
+        }
+    }
+    free(v);
+    free(g);
+    free(d);
+}
