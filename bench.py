@@ -158,6 +158,52 @@ def time_case(case, steps, warmup, dev, ws=None, mode=None, act=0, residual_seed
             "gemm_ms_p10": pct(0.1), "gemm_ms_p50": pct(0.5), "gemm_ms_p90": pct(0.9)}, ws
 
 
+def time_layernorm(dev, steps, warmup, R=16384, D=4096):
+    """The scaled LayerNorm of a 16384-token, d = 4096 transformer layer
+    (Appendix C.2): forward FP16 -> E4M3 (scale 1) and the input gradient
+    E5M2 dy, FP16 x -> E5M2 dx with the dynamic rescale (Section 4), each
+    timed with HIP events over `steps` calls. Algorithmic bytes: forward
+    R*D*(2 + 1); backward R*D*(2*(1 + 2) + 1): the statistic precedes the
+    cast, so x and dy are read twice."""
+    import torch
+    from paper_2407_17353_amd import binding as sc
+    from paper_2407_17353_amd import workloads as wl
+
+    g = torch.Generator(device="cpu").manual_seed(wl.seed_of(5, 60))
+    x = sc.ScaledArray((torch.randn((R, D), generator=g) * 1.5).to(torch.float16).view(torch.int16)
+                       .to(dev), sc.F16, sc.scale_tensor(0, dev))
+    dy = sc.ScaledArray(wl.fp8_normal((R, D), wl.E5M2, wl.seed_of(5, 61), dev), wl.E5M2,
+                        sc.scale_tensor(-8, dev))
+    gamma = (1.0 + 0.2 * torch.randn(D, generator=g)).to(dev)
+    beta = (0.1 * torch.randn(D, generator=g)).to(dev)
+    y = sc.empty_scaled(R, D, sc.E4M3, dev)
+    dx = sc.empty_scaled(R, D, sc.E5M2, dev)
+    dgamma = torch.empty(D, device=dev)
+    dbeta = torch.empty(D, device=dev)
+    ws = sc.workspace(sc.scalify_layernorm_bwd_workspace_size(R, D), dev)
+    res = {}
+    calls = {"fwd": lambda: sc.scalify_layernorm_fwd(x, y, gamma=gamma, beta=beta, eps=1e-5),
+             "bwd": lambda: sc.scalify_layernorm_bwd(dy, x, dx, gamma=gamma, eps=1e-5,
+                                                     dgamma=dgamma, dbeta=dbeta, ws=ws)}
+    nbytes = {"fwd": R * D * 3, "bwd": R * D * 7}
+    for name, fn in calls.items():
+        for _ in range(warmup):
+            fn()
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0.record()
+        for _ in range(steps):
+            fn()
+        t1.record()
+        torch.cuda.synchronize()
+        us = t0.elapsed_time(t1) / steps * 1e3
+        res[name] = {"us": round(us, 2), "GB/s": round(nbytes[name] / us / 1e3, 1),
+                     "frac_hbm": round(nbytes[name] / us / 1e3 / PEAK_HBM_GBS, 4),
+                     "alg_bytes": nbytes[name]}
+    res["shape"] = [R, D]
+    return res
+
+
 def cpu_baseline(case, target_s):
     """The oracle as it stands (fp64 accumulate + epilogue), timed on the
     first m rows of the same workload, m chosen for about target_s seconds."""
@@ -256,6 +302,7 @@ def main():
             "ms_per_step": round(rf["ms_per_step"], 4),
             "gemm_kernel_us": round(rf["gemm_ms"] * 1e3, 2),
             "epilogue_cast_us": round(rf["cast_ms"] * 1e3, 2) if m == sc.RESCALE_AMAX else None}
+    line["layernorm"] = time_layernorm(dev, 20, 10)
     if args.sweep:
         sweep = []
         for cfg, cases in wl.all_configs().items():

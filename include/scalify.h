@@ -15,6 +15,9 @@
  *     -> rebalance_scale (Section 3.3, Algorithm 4); the statistic is amax;
  *   - set_scaling and get_data_and_scale (Section 3.1);
  *   - casts act on the data component only (Appendix A, cast operators);
+ *   - the scaled add and activation rules, fused into the matmul epilogue
+ *     (Section 3.2, Algorithm 3; Appendix C.1), and the scaled LayerNorm with
+ *     the dynamic rescale of its input gradient (Appendix C.2, Section 4);
  *   - FP8 formats E4M3 / E5M2 (Section 1, Appendix A; OCP encodings on gfx950)
  *     and FP16 (E5M10) outputs.
  *
@@ -219,6 +222,55 @@ scalify_status scalify_cast(const scalify_scaled_array* in, scalify_scaled_array
  * layout rules as scalify_rescale. */
 scalify_status scalify_set_scaling(const scalify_scaled_array* in, scalify_scaled_array* out,
                                    int32_t new_scale_log2, int32_t saturate, void* stream);
+
+/* Scaled LayerNorm forward (Appendix C.2): a mean-variance normalization is
+ * invariant to the scale of its input up to its eps, so it normalizes the
+ * data component and gives the output scale 1. Per row r of x (R x D):
+ *   mean = sum_j x_d[r,j] / D,  std = sqrt(sum_j (x_d[r,j] - mean)^2 / D),
+ *   y = (x_d - mean) / (std + eps) * gamma + beta,
+ *   out.data = RNE(y) in out.dtype (saturating when saturate), *out.scale = 1.
+ * x.dtype: any scalify_dtype (x.scale is not read); out.dtype: E4M3, E5M2 or
+ * F16. Both R x D, row-major (trans = 0), rows 16-byte aligned (ld a
+ * multiple of 16 bytes, ld >= D), 1 <= D <= 8192 (any D when R = 0). gamma,
+ * beta: device fp32 [D], NULL = 1 and 0. eps >= 0 (ERR_VALUE otherwise). out
+ * may be the very same matrix as x (same data, element size and ld) but must
+ * not otherwise overlap it. pre_out: optional device fp32 [R][D] receiving y
+ * before the cast (validation). The statistics are fp32 sums in a fixed
+ * order: reruns are bit-identical. */
+scalify_status scalify_layernorm_fwd(const scalify_scaled_array* x, const float* gamma,
+                                     const float* beta, float eps, scalify_scaled_array* out,
+                                     int32_t saturate, float* pre_out, void* stream);
+
+/* Bytes of device workspace scalify_layernorm_bwd needs: a 256-byte header
+ * plus min(R, 1024) x 2 x D fp32 partial parameter gradients. 0 for invalid
+ * sizes (D > 8192). */
+size_t scalify_layernorm_bwd_workspace_size(int64_t R, int64_t D);
+
+/* Input gradient of scalify_layernorm_fwd with its dynamic rescale (the
+ * LayerNorm backward rescale of the paper's experiments, Section 4, with the
+ * rebalance of Section 3.3). The forward is a function of the data x_d =
+ * X / X_s, so for an upstream gradient dY = dy_d * s_dy the input gradient is
+ * the ScaledArray (dx, s_dy / s_x) with, per row (c = x_d - mean,
+ * s = std + eps, xhat = c / s, g = dy_d * gamma):
+ *   dx = (g - mean(g) - (c / std) mean(g * xhat)) / s   (last term 0 when std = 0).
+ * AMAX: e_r = floor(log2 amax |dx|) - target_log2 (0 for amax 0 / Inf / all
+ * NaN); NONE: e_r = 0. e_out = clamp(e(s_dy) - e(s_x) + e_r, -127, 127),
+ * dx.data = RNE(dx * 2^(e(s_dy) - e(s_x) - e_out)), *dx.scale = 2^e_out.
+ * dgamma[j] = sum_r dy_d[r,j] xhat[r,j] and dbeta[j] = sum_r dy_d[r,j]
+ * (optional device fp32 [D]; their true values are these times s_dy);
+ * amax_out: optional device fp32, the amax of |dx|; pre_out: optional device
+ * fp32 [R][D], dx before the rescale (validation). dy and x: any
+ * scalify_dtype, R x D with the layout rules of scalify_layernorm_fwd; dx:
+ * E4M3, E5M2 or F16, the same layout, may be the very same matrix as dy or x
+ * but must not otherwise overlap them. workspace: at least
+ * scalify_layernorm_bwd_workspace_size(R, D) bytes, 256-byte aligned, not
+ * shared with a concurrent call. Deterministic (fixed-order sums). */
+scalify_status scalify_layernorm_bwd(const scalify_scaled_array* dy, const scalify_scaled_array* x,
+                                     const float* gamma, float eps, scalify_scaled_array* dx,
+                                     float* dgamma, float* dbeta, int32_t rescale,
+                                     int32_t target_log2, int32_t saturate, float* amax_out,
+                                     float* pre_out, void* workspace, size_t workspace_bytes,
+                                     void* stream);
 
 /* Human-readable name of a status code (static string). */
 const char* scalify_status_string(int32_t status);

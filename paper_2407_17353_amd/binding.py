@@ -54,7 +54,8 @@ class CMatmulOpts(ctypes.Structure):
 EXPORTED = ("scalify_matmul_scale_log2", "scalify_matmul_workspace_size",
             "scalify_matmul_workspace_size_opts", "scalify_matmul",
             "scalify_rescale_workspace_size", "scalify_rescale", "scalify_cast",
-            "scalify_set_scaling", "scalify_status_string")
+            "scalify_set_scaling", "scalify_status_string", "scalify_layernorm_fwd",
+            "scalify_layernorm_bwd_workspace_size", "scalify_layernorm_bwd")
 
 _lib = None
 
@@ -88,6 +89,14 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.scalify_cast.restype = ctypes.c_int
     lib.scalify_set_scaling.argtypes = [P(CScaledArray), P(CScaledArray), i32, i32, vp]
     lib.scalify_set_scaling.restype = ctypes.c_int
+    f32 = ctypes.c_float
+    lib.scalify_layernorm_fwd.argtypes = [P(CScaledArray), vp, vp, f32, P(CScaledArray), i32, vp, vp]
+    lib.scalify_layernorm_fwd.restype = ctypes.c_int
+    lib.scalify_layernorm_bwd_workspace_size.argtypes = [i64, i64]
+    lib.scalify_layernorm_bwd_workspace_size.restype = ctypes.c_size_t
+    lib.scalify_layernorm_bwd.argtypes = [P(CScaledArray), P(CScaledArray), vp, f32, P(CScaledArray),
+                                          vp, vp, i32, i32, i32, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.scalify_layernorm_bwd.restype = ctypes.c_int
     lib.scalify_status_string.argtypes = [i32]
     lib.scalify_status_string.restype = ctypes.c_char_p
     _lib = lib
@@ -239,6 +248,51 @@ def scalify_set_scaling(x: ScaledArray, out: ScaledArray, new_scale_log2: int, *
 
 
 # ----------------------------------------------------------------------------- helpers
+
+def _ptr_or_none(t: Optional[torch.Tensor]):
+    return t.data_ptr() if t is not None else None
+
+
+def scalify_layernorm_fwd(x: ScaledArray, out: ScaledArray, *, gamma: torch.Tensor = None,
+                          beta: torch.Tensor = None, eps: float = 1e-5, saturate: bool = True,
+                          pre_out: torch.Tensor = None, stream=None) -> None:
+    """Scaled LayerNorm forward (Appendix C.2): normalizes x's data, output
+    scale 1; see scalify_layernorm_fwd in include/scalify.h. gamma, beta:
+    fp32 [D] device tensors or None."""
+    lib = load_library()
+    cx, co = x.c_struct(), out.c_struct()
+    st = lib.scalify_layernorm_fwd(ctypes.byref(cx), _ptr_or_none(gamma), _ptr_or_none(beta),
+                                   float(eps), ctypes.byref(co), int(bool(saturate)),
+                                   _ptr_or_none(pre_out), _stream_handle(stream))
+    _check(st, "scalify_layernorm_fwd")
+
+
+def scalify_layernorm_bwd_workspace_size(R: int, D: int) -> int:
+    return int(load_library().scalify_layernorm_bwd_workspace_size(R, D))
+
+
+def scalify_layernorm_bwd(dy: ScaledArray, x: ScaledArray, dx: ScaledArray, *,
+                          gamma: torch.Tensor = None, eps: float = 1e-5,
+                          rescale: int = RESCALE_AMAX, target_log2: int = 0,
+                          saturate: bool = True, dgamma: torch.Tensor = None,
+                          dbeta: torch.Tensor = None, amax_out: torch.Tensor = None,
+                          pre_out: torch.Tensor = None, ws: torch.Tensor = None,
+                          stream=None) -> None:
+    """LayerNorm input gradient with its dynamic rescale (Section 4, Section
+    3.3); see scalify_layernorm_bwd in include/scalify.h."""
+    lib = load_library()
+    R, D = x.shape
+    if ws is None:
+        ws = workspace(scalify_layernorm_bwd_workspace_size(R, D), x.data.device)
+    cdy, cx, cdx = dy.c_struct(), x.c_struct(), dx.c_struct()
+    st = lib.scalify_layernorm_bwd(ctypes.byref(cdy), ctypes.byref(cx), _ptr_or_none(gamma),
+                                   float(eps), ctypes.byref(cdx), _ptr_or_none(dgamma),
+                                   _ptr_or_none(dbeta), int(rescale), int(target_log2),
+                                   int(bool(saturate)), _ptr_or_none(amax_out),
+                                   _ptr_or_none(pre_out), ws.data_ptr(), ws.numel(),
+                                   _stream_handle(stream))
+    _check(st, "scalify_layernorm_bwd")
+
 
 def empty_scaled(rows: int, cols: int, fmt: int, device, ld: int = None) -> ScaledArray:
     """Output ScaledArray [rows, cols] with leading dimension ld (default: cols

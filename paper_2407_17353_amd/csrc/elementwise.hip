@@ -11,11 +11,10 @@
 // Every kernel moves 16 elements per thread per iteration with 128-bit
 // loads and stores and walks the array with a grid-stride loop.
 #include "codec.h"
+#include "ew_util.h"
 #include "kernels.h"
 
 namespace scalify {
-
-typedef unsigned int u4 __attribute__((ext_vector_type(4)));
 
 constexpr int EW_THREADS = 256;
 
@@ -72,115 +71,6 @@ __global__ void finalize_amax_kernel(const uint32_t* hdr, int e_c, float* amax_o
 hipError_t launch_finalize_amax(const uint32_t* hdr, int e_c, float* amax_out, hipStream_t s) {
   hipLaunchKernelGGL(finalize_amax_kernel, dim3(1), dim3(64), 0, s, hdr, e_c, amax_out);
   return hipGetLastError();
-}
-
-// Load 16 consecutive elements of format F as raw codes / fp32 bits.
-template <int F>
-__device__ __forceinline__ void load16(const void* base, int64_t e, uint32_t (&c)[16]) {
-  if (F == kE4M3 || F == kE5M2) {
-    const u4 v = *(const u4*)((const uint8_t*)base + e);
-#pragma unroll
-    for (int i = 0; i < 16; ++i) c[i] = (v[i >> 2] >> (8 * (i & 3))) & 0xFFu;
-  } else if (F == kF16) {
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const u4 v = *(const u4*)((const uint16_t*)base + e + 8 * h);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) c[8 * h + i] = (v[i >> 1] >> (16 * (i & 1))) & 0xFFFFu;
-    }
-  } else {
-#pragma unroll
-    for (int h = 0; h < 4; ++h) {
-      const u4 v = *(const u4*)((const uint32_t*)base + e + 4 * h);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) c[4 * h + i] = v[i];
-    }
-  }
-}
-
-template <int F>
-__device__ __forceinline__ uint32_t load1(const void* base, int64_t e) {
-  if (F == kE4M3 || F == kE5M2) return ((const uint8_t*)base)[e];
-  if (F == kF16) return ((const uint16_t*)base)[e];
-  return ((const uint32_t*)base)[e];
-}
-
-template <int F>
-__device__ __forceinline__ uint32_t to_bits(uint32_t c) {
-  if constexpr (F == kF32) return c;
-  else return decode_bits<F>(c);
-}
-
-template <int F>
-__device__ __forceinline__ void store16(void* base, int64_t e, const uint32_t (&c)[16]) {
-  if (F == kF16) {
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      u4 v;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) v[i] = c[8 * h + 2 * i] | (c[8 * h + 2 * i + 1] << 16);
-      *(u4*)((uint16_t*)base + e + 8 * h) = v;
-    }
-  } else {
-    u4 v;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      v[i] = c[4 * i] | (c[4 * i + 1] << 8) | (c[4 * i + 2] << 16) | (c[4 * i + 3] << 24);
-    *(u4*)((uint8_t*)base + e) = v;
-  }
-}
-
-template <int F>
-__device__ __forceinline__ void store1(void* base, int64_t e, uint32_t c) {
-  if (F == kF16) ((uint16_t*)base)[e] = (uint16_t)c;
-  else ((uint8_t*)base)[e] = (uint8_t)c;
-}
-
-// 16 fp32 values (bits) times 2^-shift -> 16 codes packed in 4 words (FP8)
-// or 8 words (FP16: two codes per word). FP8 uses the hardware conversion
-// when `fast` (the shift is in the window where it is exact, fp32
-// subnormal inputs included) and no value is NaN, else the integer cast.
-template <int OUTF>
-__device__ __forceinline__ void encode16(const uint32_t (&u)[16], int shift, float scale, bool fast,
-                                         bool sat, uint32_t (&w)[8]) {
-  if (OUTF == kE4M3 || OUTF == kE5M2) {
-    bool nan = false;
-#pragma unroll
-    for (int i = 0; i < 16; ++i) nan |= is_nan_bits(u[i]);
-    if (fast && !nan) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-        w[q] = cast4_fp8_hw<OUTF>(u[4 * q], u[4 * q + 1], u[4 * q + 2], u[4 * q + 3], scale, sat);
-    } else {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        w[q] = 0;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) w[q] |= cast_bits<OUTF>(u[4 * q + i], shift, sat) << (8 * i);
-      }
-    }
-  } else {
-#pragma unroll
-    for (int q = 0; q < 8; ++q)
-      w[q] = cast_bits<OUTF>(u[2 * q], shift, sat) | (cast_bits<OUTF>(u[2 * q + 1], shift, sat) << 16);
-  }
-}
-
-template <int OUTF>
-__device__ __forceinline__ void store_words16(void* base, int64_t e, const uint32_t (&w)[8]) {
-  if (OUTF == kF16) {
-    *(u4*)((uint16_t*)base + e) = u4{w[0], w[1], w[2], w[3]};
-    *(u4*)((uint16_t*)base + e + 8) = u4{w[4], w[5], w[6], w[7]};
-  } else {
-    *(u4*)((uint8_t*)base + e) = u4{w[0], w[1], w[2], w[3]};
-  }
-}
-
-// Element i of the packed words.
-template <int OUTF>
-__device__ __forceinline__ uint32_t word_code(const uint32_t (&w)[8], int i) {
-  if (OUTF == kF16) return (w[i >> 1] >> (16 * (i & 1))) & 0xFFFFu;
-  return (w[i >> 2] >> (8 * (i & 3))) & 0xFFu;
 }
 
 // ---------------------------------------------------------------- GEMM epilogue cast

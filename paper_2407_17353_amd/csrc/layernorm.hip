@@ -1,0 +1,390 @@
+// Scaled LayerNorm (Appendix C.2) and its input gradient with the dynamic
+// rescale (the LayerNorm backward rescale of the experiments, Section 4).
+//
+// Forward: a mean-variance normalization is scale invariant up to its eps,
+// so the data component X_d is normalized and the output gets scale 1:
+//   xhat = (x - mean) / (std + eps),  y = xhat * gamma + beta,  cast(y).
+// Backward: the gradient with respect to X_d, as the ScaledArray
+// (dx, s_dy / s_x), then rebalanced by the amax rule and cast:
+//   dx = (g - mean(g) - (c / std) mean(g * xhat)) / (std + eps),  g = dy * gamma,
+//   c = x - mean; dgamma = sum_rows dy * xhat, dbeta = sum_rows dy.
+//
+// Row statistics: one wave per row; lane l takes the 16-column chunks l,
+// l + 64, ... of the row, and the row sums are lane sums then a wave
+// butterfly (no LDS, no barrier; fixed order, so reruns are bit-identical).
+// Each pass over the row re-reads it (the later passes are served by the
+// caches) so that a wave holds little and many rows are in flight. The
+// forward's last pass writes y. The backward's statistic kernel also streams
+// dy (twice: for mean(g), mean(g * xhat), then for dx's amax) and keeps, per
+// row, the four numbers dx needs; its apply kernel is then a streaming pass over
+// 32-row x 2048-column tiles that casts dx with the rescale the global amax
+// gives and accumulates the tile's partial parameter gradients, which a last
+// kernel sums over the row tiles in a fixed order.
+#include "codec.h"
+#include "ew_util.h"
+#include "layernorm.h"
+
+namespace scalify {
+
+constexpr int LN_THREADS = 256;   // 4 waves: 4 rows at a time
+constexpr int LN_TILE_ROWS = 32;  // apply kernel: rows per workgroup
+constexpr int LN_TILE_THREADS = 128;
+constexpr int LN_TILE_COLS = 16 * LN_TILE_THREADS;
+
+template <int F>
+__device__ __forceinline__ void ln_chunk_f(const void* base, int64_t off, int valid,
+                                           float (&v)[16]) {
+  uint32_t c[16];
+  if (valid >= 16) {
+    load16<F>(base, off, c);
+  } else {
+    // ragged end of the row: element loads at clamped (valid) addresses
+#pragma unroll
+    for (int i = 0; i < 16; ++i) c[i] = load1<F>(base, off + (i < valid ? i : 0));
+  }
+#pragma unroll
+  for (int i = 0; i < 16; ++i) v[i] = i < valid ? decode_hw<F>(c[i]) : 0.0f;
+}
+
+// 16 values of a row from column n (columns >= D read as 0), format fmt.
+__device__ __forceinline__ void ln_load16(int fmt, const void* base, int64_t off, int valid,
+                                          float (&v)[16]) {
+  if (fmt == kF16) ln_chunk_f<kF16>(base, off, valid, v);
+  else if (fmt == kE4M3) ln_chunk_f<kE4M3>(base, off, valid, v);
+  else if (fmt == kE5M2) ln_chunk_f<kE5M2>(base, off, valid, v);
+  else ln_chunk_f<kF32>(base, off, valid, v);
+}
+
+__device__ __forceinline__ void ln_param16(const float* p, int n, int valid, float dflt,
+                                           float (&v)[16]) {
+  if (p == nullptr) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) v[i] = dflt;
+  } else if (valid >= 16) {
+    ln_chunk_f<kF32>(p, n, 16, v);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) v[i] = i < valid ? p[n + i] : dflt;
+  }
+}
+
+__device__ __forceinline__ float wave_sum(float a) {
+  for (int off = 32; off > 0; off >>= 1) a += __shfl_xor(a, off, 64);
+  return a;
+}
+
+// Cast and store 16 values of one row at column n.
+template <int OUTF>
+__device__ __forceinline__ void ln_store16(void* out, int64_t off, int valid, const float (&y)[16],
+                                           int shift, float scale, bool fast, bool sat) {
+  uint32_t u[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) u[i] = __float_as_uint(y[i]);
+  uint32_t w[8];
+  encode16<OUTF>(u, shift, scale, fast, sat, w);
+  if (valid >= 16) {
+    store_words16<OUTF>(out, off, w);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      if (i < valid) store1<OUTF>(out, off + i, word_code<OUTF>(w, i));
+  }
+}
+
+__device__ __forceinline__ void ln_store_f32(float* q, int valid, const float (&y)[16]) {
+  if (valid >= 16 && ((uintptr_t)q & 15u) == 0) {
+#pragma unroll
+    for (int h = 0; h < 4; ++h) *(u4*)(q + 4 * h) = u4{__float_as_uint(y[4 * h]), __float_as_uint(y[4 * h + 1]),
+                                                         __float_as_uint(y[4 * h + 2]), __float_as_uint(y[4 * h + 3])};
+  } else {
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      if (i < valid) q[i] = y[i];
+  }
+}
+
+// Mean and std of row r (fp32; lane sums over its chunks, then a wave
+// butterfly): two passes over the row, the second one served by the caches.
+template <int XF>
+__device__ __forceinline__ void ln_row_stats(const LnParams& p, int64_t r, int lane, float& mu,
+                                             float& sigma) {
+  const int nch = (p.D + 15) / 16;
+  float s = 0.0f;
+#pragma unroll 2
+  for (int q = lane; q < nch; q += 64) {
+    float v[16];
+    ln_chunk_f<XF>(p.x, r * p.ldx + 16 * q, p.D - 16 * q, v);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) s += v[i];  // columns >= D read as 0
+  }
+  mu = wave_sum(s) / (float)p.D;
+  float t = 0.0f;
+#pragma unroll 2
+  for (int q = lane; q < nch; q += 64) {
+    float v[16];
+    const int valid = p.D - 16 * q;
+    ln_chunk_f<XF>(p.x, r * p.ldx + 16 * q, valid, v);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const float d = v[i] - mu;
+      t += i < valid ? d * d : 0.0f;
+    }
+  }
+  sigma = sqrtf(wave_sum(t) / (float)p.D);
+}
+
+template <int XF, int OUTF>
+__global__ __launch_bounds__(LN_THREADS) void ln_fwd_kernel(LnParams p) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const bool sat = p.sat != 0;
+  const int nch = (p.D + 15) / 16;
+  if (blockIdx.x == 0 && threadIdx.x == 0) *p.out_scale = 1.0f;  // Appendix C.2: scale 1
+#pragma unroll 1
+  for (int64_t r = (int64_t)blockIdx.x * 4 + wave; r < p.R; r += (int64_t)gridDim.x * 4) {
+    float mu, sigma;
+    ln_row_stats<XF>(p, r, lane, mu, sigma);
+    const float inv = 1.0f / (sigma + p.eps);
+#pragma unroll 1
+    for (int q = lane; q < nch; q += 64) {
+      const int n = 16 * q;
+      const int valid = p.D - n;
+      float v[16], g[16], b[16], y[16];
+      ln_chunk_f<XF>(p.x, r * p.ldx + n, valid, v);
+      ln_param16(p.gamma, n, valid, 1.0f, g);
+      ln_param16(p.beta, n, valid, 0.0f, b);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) y[i] = (v[i] - mu) * inv * g[i] + b[i];
+      if (p.pre_out) ln_store_f32(p.pre_out + r * (int64_t)p.D + n, valid, y);
+      ln_store16<OUTF>(p.out, r * p.ldo + n, valid, y, 0, 1.0f, true, sat);
+    }
+  }
+}
+
+// Per-row numbers of the gradient (rowstats[r] = {mean, 1/(std+eps), mean(g),
+// mean(g * xhat)/std or 0}), so that dx = (dy gamma - mean(g) - (x - mean) t) * inv.
+// Both backward kernels evaluate it with this code and no contraction, so the
+// apply kernel casts bit for bit the values whose amax the statistic measured.
+__device__ __forceinline__ float ln_dx(float x, float dy, float gam, const float4& st) {
+#pragma clang fp contract(off)
+  const float g = dy * gam;
+  return (g - st.z - (x - st.x) * st.w) * st.y;
+}
+
+template <int XF>
+__global__ __launch_bounds__(LN_THREADS) void ln_bwd_stats_kernel(LnParams p) {
+  __shared__ float wmax[4];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int nch = (p.D + 15) / 16;
+  float lmax = 0.0f;
+  float4* rowstats = (float4*)p.partial;
+#pragma unroll 1
+  for (int64_t r = (int64_t)blockIdx.x * 4 + wave; r < p.R; r += (int64_t)gridDim.x * 4) {
+    float mu, sigma;
+    ln_row_stats<XF>(p, r, lane, mu, sigma);
+    const float inv = 1.0f / (sigma + p.eps);
+    float sg = 0.0f, sgx = 0.0f;
+#pragma unroll 1
+    for (int q = lane; q < nch; q += 64) {
+      const int n = 16 * q;
+      const int valid = p.D - n;
+      float v[16], d[16], gam[16];
+      ln_chunk_f<XF>(p.x, r * p.ldx + n, valid, v);
+      ln_load16(p.dy_fmt, p.dy, r * p.lddy + n, valid, d);
+      ln_param16(p.gamma, n, valid, 1.0f, gam);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const float g = i < valid ? d[i] * gam[i] : 0.0f;
+        sg += g;
+        sgx += g * ((v[i] - mu) * inv);
+      }
+    }
+    sg = wave_sum(sg);
+    sgx = wave_sum(sgx);
+    float4 st;
+    st.x = mu;
+    st.y = inv;
+    st.z = sg / (float)p.D;
+    st.w = sigma > 0.0f ? (sgx / (float)p.D) / sigma : 0.0f;
+    if (lane == 0) rowstats[r] = st;
+#pragma unroll 1
+    for (int q = lane; q < nch; q += 64) {
+      const int n = 16 * q;
+      const int valid = p.D - n;
+      float v[16], d[16], gam[16], dx[16];
+      ln_chunk_f<XF>(p.x, r * p.ldx + n, valid, v);
+      ln_load16(p.dy_fmt, p.dy, r * p.lddy + n, valid, d);
+      ln_param16(p.gamma, n, valid, 1.0f, gam);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        dx[i] = ln_dx(v[i], d[i], gam[i], st);
+        if (i < valid) lmax = fmaxf(lmax, fabsf(dx[i]));  // fmaxf skips NaN
+      }
+      if (p.pre_out) ln_store_f32(p.pre_out + r * (int64_t)p.D + n, valid, dx);
+    }
+  }
+  // amax of |dx|: wave butterfly, the four waves, one atomic max per workgroup
+  for (int off = 32; off > 0; off >>= 1) lmax = fmaxf(lmax, __shfl_xor(lmax, off, 64));
+  if (lane == 0) wmax[wave] = lmax;
+  __syncthreads();
+  if (threadIdx.x == 0)
+    atomicMax(p.hdr, __float_as_uint(fmaxf(fmaxf(wmax[0], wmax[1]), fmaxf(wmax[2], wmax[3]))));
+}
+
+// Tile (row block blockIdx.y of LN_TILE_ROWS rows, column block blockIdx.x of
+// LN_TILE_COLS columns): dx recomputed from the row numbers, cast with the
+// rescale, and the tile's partial parameter gradients.
+template <int XF, int DYF, int OUTF>
+__global__ __launch_bounds__(LN_TILE_THREADS) void ln_bwd_apply_kernel(LnParams p) {
+  const int e_in = (int)p.hdr[1];
+  int e_r = 0;
+  if (p.mode == 1) e_r = rescale_exponent(p.hdr[0], p.target);
+  const int e_out = clamp_e8m0(e_in + e_r);
+  const int shift = e_out - e_in;
+  if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) {
+    *p.out_scale = pow2_float(e_out);
+    if (p.amax_out) *p.amax_out = __uint_as_float(p.hdr[0]);
+  }
+  const bool sat = p.sat != 0;
+  const bool fast = shift >= kFastShiftMinSub && shift <= kFastShiftMax;
+  const float scale = fast ? pow2_float(shift) : 1.0f;
+  const int n = (int)blockIdx.x * LN_TILE_COLS + 16 * (int)threadIdx.x;
+  const int valid = p.D - n;
+  const float4* rowstats = (const float4*)p.partial;
+  const int64_t dp = layernorm_param_stride(p.D);
+  float* part = p.partial + 4 * p.R + (int64_t)blockIdx.y * 2 * dp;
+  if (valid <= 0) return;
+  float gam[16], pg[16], pb[16];
+  ln_param16(p.gamma, n, valid, 1.0f, gam);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) pg[i] = pb[i] = 0.0f;
+  const int64_t r0 = (int64_t)blockIdx.y * LN_TILE_ROWS;
+  const int64_t r1 = r0 + LN_TILE_ROWS < p.R ? r0 + LN_TILE_ROWS : p.R;
+#pragma unroll 1
+  for (int64_t r = r0; r < r1; ++r) {
+    const float4 st = rowstats[r];
+    float x[16], d[16], dx[16];
+    ln_chunk_f<XF>(p.x, r * p.ldx + n, valid, x);
+    ln_chunk_f<DYF>(p.dy, r * p.lddy + n, valid, d);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      dx[i] = ln_dx(x[i], d[i], gam[i], st);
+      pg[i] += d[i] * ((x[i] - st.x) * st.y);
+      pb[i] += d[i];
+    }
+    ln_store16<OUTF>(p.out, r * p.ldo + n, valid, dx, shift, scale, fast, sat);
+  }
+  if (p.dgamma || p.dbeta) {
+    ln_store_f32(part + n, valid, pg);
+    ln_store_f32(part + dp + n, valid, pb);
+  }
+}
+
+// dgamma[j], dbeta[j] = fixed-order sums of the row tiles' partials: a
+// workgroup covers 64 columns; its 4 waves sum interleaved quarters of the
+// tiles (wave w: tiles w, w + 4, ...), then wave 0 adds the four in order.
+__global__ __launch_bounds__(256) void ln_params_kernel(const float* part, int tiles, int D,
+                                                        float* dgamma, float* dbeta) {
+  __shared__ float red[2][4][64];
+  const int c = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int j = blockIdx.x * 64 + c;
+  const int64_t dp = layernorm_param_stride(D);
+  float g = 0.0f, b = 0.0f;
+  if (j < D) {
+#pragma unroll 8
+    for (int k = w; k < tiles; k += 4) {
+      g += part[(int64_t)k * 2 * dp + j];
+      b += part[(int64_t)k * 2 * dp + dp + j];
+    }
+  }
+  red[0][w][c] = g;
+  red[1][w][c] = b;
+  __syncthreads();
+  if (w == 0 && j < D) {
+    const float sg = (red[0][0][c] + red[0][1][c]) + (red[0][2][c] + red[0][3][c]);
+    const float sb = (red[1][0][c] + red[1][1][c]) + (red[1][2][c] + red[1][3][c]);
+    if (dgamma) dgamma[j] = sg;
+    if (dbeta) dbeta[j] = sb;
+  }
+}
+
+// hdr[0] = 0 (amax), hdr[1] = e(s_dy) - e(s_x): the gradient's scale exponent.
+__global__ void ln_bwd_prologue_kernel(uint32_t* hdr, const float* s_dy, const float* s_x) {
+  if (threadIdx.x == 0) {
+    hdr[0] = 0u;
+    hdr[1] = (uint32_t)(pow2_exponent(s_dy) - pow2_exponent(s_x));
+  }
+}
+
+static int row_grid(int64_t R) {
+  const int64_t b = (R + 3) / 4;
+  return (int)(b < 1 ? 1 : (b > 8192 ? 8192 : b));
+}
+
+int64_t layernorm_row_tiles(int64_t R) {
+  const int64_t t = (R + LN_TILE_ROWS - 1) / LN_TILE_ROWS;
+  return t < 1 ? 1 : t;
+}
+
+int64_t layernorm_ws_floats(int64_t R, int64_t D) {
+  return 4 * R + layernorm_row_tiles(R) * 2 * layernorm_param_stride(D);
+}
+
+template <int XF>
+static void launch_fwd_xf(const LnParams& p, int out_dtype, hipStream_t s) {
+  const dim3 g(row_grid(p.R)), b(LN_THREADS);
+  if (out_dtype == kE4M3) hipLaunchKernelGGL((ln_fwd_kernel<XF, kE4M3>), g, b, 0, s, p);
+  else if (out_dtype == kE5M2) hipLaunchKernelGGL((ln_fwd_kernel<XF, kE5M2>), g, b, 0, s, p);
+  else hipLaunchKernelGGL((ln_fwd_kernel<XF, kF16>), g, b, 0, s, p);
+}
+
+hipError_t launch_layernorm_fwd(const LnParams& p, int out_dtype, hipStream_t s) {
+  if (p.x_fmt == kF16) launch_fwd_xf<kF16>(p, out_dtype, s);
+  else if (p.x_fmt == kF32) launch_fwd_xf<kF32>(p, out_dtype, s);
+  else if (p.x_fmt == kE4M3) launch_fwd_xf<kE4M3>(p, out_dtype, s);
+  else launch_fwd_xf<kE5M2>(p, out_dtype, s);
+  return hipGetLastError();
+}
+
+template <int XF, int DYF>
+static void launch_apply(const LnParams& p, int out_dtype, dim3 g, dim3 b, hipStream_t s) {
+  if (out_dtype == kE4M3) hipLaunchKernelGGL((ln_bwd_apply_kernel<XF, DYF, kE4M3>), g, b, 0, s, p);
+  else if (out_dtype == kE5M2) hipLaunchKernelGGL((ln_bwd_apply_kernel<XF, DYF, kE5M2>), g, b, 0, s, p);
+  else hipLaunchKernelGGL((ln_bwd_apply_kernel<XF, DYF, kF16>), g, b, 0, s, p);
+}
+
+template <int XF>
+static void launch_apply_x(const LnParams& p, int out_dtype, dim3 g, dim3 b, hipStream_t s) {
+  if (p.dy_fmt == kF16) launch_apply<XF, kF16>(p, out_dtype, g, b, s);
+  else if (p.dy_fmt == kF32) launch_apply<XF, kF32>(p, out_dtype, g, b, s);
+  else if (p.dy_fmt == kE4M3) launch_apply<XF, kE4M3>(p, out_dtype, g, b, s);
+  else launch_apply<XF, kE5M2>(p, out_dtype, g, b, s);
+}
+
+hipError_t launch_layernorm_bwd(const LnParams& p, const float* s_dy, const float* s_x,
+                                int out_dtype, hipStream_t s) {
+  hipLaunchKernelGGL(ln_bwd_prologue_kernel, dim3(1), dim3(64), 0, s, p.hdr, s_dy, s_x);
+  if (p.R > 0) {
+    const dim3 g(row_grid(p.R)), b(LN_THREADS);
+    if (p.x_fmt == kF16) hipLaunchKernelGGL((ln_bwd_stats_kernel<kF16>), g, b, 0, s, p);
+    else if (p.x_fmt == kF32) hipLaunchKernelGGL((ln_bwd_stats_kernel<kF32>), g, b, 0, s, p);
+    else if (p.x_fmt == kE4M3) hipLaunchKernelGGL((ln_bwd_stats_kernel<kE4M3>), g, b, 0, s, p);
+    else hipLaunchKernelGGL((ln_bwd_stats_kernel<kE5M2>), g, b, 0, s, p);
+  }
+  // The apply kernel also writes the output scale: at least one workgroup.
+  const int64_t tiles = layernorm_row_tiles(p.R);
+  const int cols = (p.D + LN_TILE_COLS - 1) / LN_TILE_COLS;
+  const dim3 ga(cols < 1 ? 1 : cols, (unsigned)tiles);
+  const dim3 ba(LN_TILE_THREADS);
+  if (p.x_fmt == kF16) launch_apply_x<kF16>(p, out_dtype, ga, ba, s);
+  else if (p.x_fmt == kF32) launch_apply_x<kF32>(p, out_dtype, ga, ba, s);
+  else if (p.x_fmt == kE4M3) launch_apply_x<kE4M3>(p, out_dtype, ga, ba, s);
+  else launch_apply_x<kE5M2>(p, out_dtype, ga, ba, s);
+  if ((p.dgamma || p.dbeta) && p.D > 0)
+    hipLaunchKernelGGL(ln_params_kernel, dim3((p.D + 63) / 64), dim3(256), 0, s, p.partial + 4 * p.R,
+                       (int)tiles, p.D, p.dgamma, p.dbeta);
+  return hipGetLastError();
+}
+
+}  // namespace scalify

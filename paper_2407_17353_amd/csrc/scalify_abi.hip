@@ -6,6 +6,7 @@
 
 #include "../../include/scalify.h"
 #include "kernels.h"
+#include "layernorm.h"
 
 using namespace scalify;
 
@@ -88,6 +89,38 @@ scalify_status check_elementwise(const scalify_scaled_array* in, const scalify_s
   if (i0 < o1 && o0 < i1 && !(i0 == o0 && elem_bytes(in->dtype) == elem_bytes(out->dtype)))
     return SCALIFY_ERR_LAYOUT;
   return SCALIFY_OK;
+}
+
+// A LayerNorm operand: R x D, row-major (trans = 0), 1 <= D <= 8192 when
+// R > 0, rows 16-byte aligned (ld a multiple of 16 bytes), ld >= D.
+scalify_status check_rows(const scalify_scaled_array* x, int64_t R, int64_t D) {
+  if (x->rows != R || x->cols != D) return SCALIFY_ERR_SHAPE;
+  if (x->trans != 0) return SCALIFY_ERR_LAYOUT;
+  if (R == 0) return SCALIFY_OK;
+  if (x->data == nullptr) return SCALIFY_ERR_NULL;
+  if (x->ld < D) return SCALIFY_ERR_SHAPE;
+  if ((x->ld * elem_bytes(x->dtype)) % 16 != 0 || !aligned16(x->data)) return SCALIFY_ERR_ALIGN;
+  return SCALIFY_OK;
+}
+
+// An output may be the very same matrix as an input (same data, element
+// size and ld: every row is read before it is written, by one workgroup),
+// or must not overlap it.
+bool rows_conflict(const scalify_scaled_array* a, const scalify_scaled_array* b, int64_t R,
+                   int64_t D) {
+  if (R == 0 || D == 0) return false;
+  const uintptr_t a0 = (uintptr_t)a->data;
+  const uintptr_t a1 = a0 + (uintptr_t)(((R - 1) * a->ld + D) * elem_bytes(a->dtype));
+  const uintptr_t b0 = (uintptr_t)b->data;
+  const uintptr_t b1 = b0 + (uintptr_t)(((R - 1) * b->ld + D) * elem_bytes(b->dtype));
+  const bool same = a->data == b->data && elem_bytes(a->dtype) == elem_bytes(b->dtype) &&
+                    a->ld == b->ld;
+  return a0 < b1 && b0 < a1 && !same;
+}
+
+size_t layernorm_bwd_ws(int64_t R, int64_t D) {
+  if (R < 0 || D < 0 || D > kLayerNormMaxD || R > kMaxDim) return 0;
+  return kHeaderBytes + (size_t)layernorm_ws_floats(R, D) * sizeof(float);
 }
 
 }  // namespace
@@ -311,6 +344,95 @@ scalify_status scalify_set_scaling(const scalify_scaled_array* in, scalify_scale
   p.in_scale = in->scale;
   p.out_scale = out->scale;
   if (launch_elementwise(p, in->dtype, out->dtype, (hipStream_t)stream) != hipSuccess)
+    return SCALIFY_ERR_HIP;
+  return SCALIFY_OK;
+}
+
+scalify_status scalify_layernorm_fwd(const scalify_scaled_array* x, const float* gamma,
+                                     const float* beta, float eps, scalify_scaled_array* out,
+                                     int32_t saturate, float* pre_out, void* stream) {
+  if (!x || !out) return SCALIFY_ERR_NULL;
+  if (!out->scale) return SCALIFY_ERR_NULL;
+  if (!is_any(x->dtype) || !is_out(out->dtype)) return SCALIFY_ERR_DTYPE;
+  const int64_t R = x->rows, D = x->cols;
+  if (R < 0 || D < 0 || R > kMaxDim) return SCALIFY_ERR_SHAPE;
+  if (R > 0 && (D < 1 || D > kLayerNormMaxD)) return SCALIFY_ERR_SHAPE;
+  if (!(eps >= 0.0f) || !(eps < 3.0e38f)) return SCALIFY_ERR_VALUE;
+  if (!aligned16(gamma) || !aligned16(beta) || !aligned16(pre_out)) return SCALIFY_ERR_ALIGN;
+  scalify_status st;
+  if ((st = check_rows(x, R, D)) != SCALIFY_OK) return st;
+  if ((st = check_rows(out, R, D)) != SCALIFY_OK) return st;
+  if (rows_conflict(x, out, R, D)) return SCALIFY_ERR_LAYOUT;
+  LnParams p = {};
+  p.x = x->data;
+  p.ldx = x->ld;
+  p.x_fmt = x->dtype;
+  p.gamma = gamma;
+  p.beta = beta;
+  p.out = out->data;
+  p.ldo = out->ld;
+  p.pre_out = pre_out;
+  p.R = R;
+  p.D = (int)D;
+  p.eps = eps;
+  p.sat = saturate != 0;
+  p.out_scale = out->scale;
+  if (launch_layernorm_fwd(p, out->dtype, (hipStream_t)stream) != hipSuccess)
+    return SCALIFY_ERR_HIP;
+  return SCALIFY_OK;
+}
+
+size_t scalify_layernorm_bwd_workspace_size(int64_t R, int64_t D) { return layernorm_bwd_ws(R, D); }
+
+scalify_status scalify_layernorm_bwd(const scalify_scaled_array* dy, const scalify_scaled_array* x,
+                                     const float* gamma, float eps, scalify_scaled_array* dx,
+                                     float* dgamma, float* dbeta, int32_t rescale,
+                                     int32_t target_log2, int32_t saturate, float* amax_out,
+                                     float* pre_out, void* workspace, size_t workspace_bytes,
+                                     void* stream) {
+  if (!dy || !x || !dx) return SCALIFY_ERR_NULL;
+  if (!dx->scale) return SCALIFY_ERR_NULL;
+  if (!is_any(dy->dtype) || !is_any(x->dtype) || !is_out(dx->dtype)) return SCALIFY_ERR_DTYPE;
+  if (rescale != SCALIFY_RESCALE_NONE && rescale != SCALIFY_RESCALE_AMAX) return SCALIFY_ERR_VALUE;
+  if (target_log2 < -1000 || target_log2 > 1000) return SCALIFY_ERR_VALUE;
+  if (!(eps >= 0.0f) || !(eps < 3.0e38f)) return SCALIFY_ERR_VALUE;
+  const int64_t R = x->rows, D = x->cols;
+  if (R < 0 || D < 0 || R > kMaxDim) return SCALIFY_ERR_SHAPE;
+  if (R > 0 && (D < 1 || D > kLayerNormMaxD)) return SCALIFY_ERR_SHAPE;
+  if (!aligned16(gamma) || !aligned16(dgamma) || !aligned16(dbeta) || !aligned16(pre_out))
+    return SCALIFY_ERR_ALIGN;
+  scalify_status st;
+  if ((st = check_rows(x, R, D)) != SCALIFY_OK) return st;
+  if ((st = check_rows(dy, R, D)) != SCALIFY_OK) return st;
+  if ((st = check_rows(dx, R, D)) != SCALIFY_OK) return st;
+  if (rows_conflict(dx, dy, R, D) || rows_conflict(dx, x, R, D)) return SCALIFY_ERR_LAYOUT;
+  const size_t need = layernorm_bwd_ws(R, D);
+  if (!workspace || workspace_bytes < need || ((uintptr_t)workspace & 255u))
+    return SCALIFY_ERR_WORKSPACE;
+  LnParams p = {};
+  p.x = x->data;
+  p.ldx = x->ld;
+  p.x_fmt = x->dtype;
+  p.dy = dy->data;
+  p.lddy = dy->ld;
+  p.dy_fmt = dy->dtype;
+  p.gamma = gamma;
+  p.out = dx->data;
+  p.ldo = dx->ld;
+  p.pre_out = pre_out;
+  p.R = R;
+  p.D = (int)D;
+  p.eps = eps;
+  p.sat = saturate != 0;
+  p.target = target_log2;
+  p.mode = rescale == SCALIFY_RESCALE_AMAX ? 1 : 0;
+  p.hdr = (uint32_t*)workspace;
+  p.partial = (float*)((uint8_t*)workspace + kHeaderBytes);
+  p.out_scale = dx->scale;
+  p.amax_out = amax_out;
+  p.dgamma = dgamma;
+  p.dbeta = dbeta;
+  if (launch_layernorm_bwd(p, dy->scale, x->scale, dx->dtype, (hipStream_t)stream) != hipSuccess)
     return SCALIFY_ERR_HIP;
   return SCALIFY_OK;
 }

@@ -222,3 +222,84 @@ def test_matmul_fused_argument_errors(case, status):
         opts = fused_opts(res)
         kw["ws_bytes"] = sc.scalify_matmul_workspace_size(64, 32, sc.E4M3)
     assert call_matmul(a, b, out, opts=opts, **kw) == status
+
+
+def _ln_fwd(x, out, gamma=None, beta=None, eps=1e-5, pre=None):
+    lib = sc.load_library()
+    return lib.scalify_layernorm_fwd(ctypes.byref(x), gamma, beta, eps, ctypes.byref(out), 1, pre, None)
+
+
+def _ln_bwd(dy, x, dx, mode=sc.RESCALE_AMAX, eps=1e-5, ws=FAKE + 8192, ws_bytes=1 << 40, **kw):
+    lib = sc.load_library()
+    return lib.scalify_layernorm_bwd(ctypes.byref(dy), ctypes.byref(x), kw.get("gamma"), eps,
+                                     ctypes.byref(dx), kw.get("dgamma"), kw.get("dbeta"), mode, 0, 1,
+                                     None, kw.get("pre"), ws, ws_bytes, None)
+
+
+def test_layernorm_workspace_size():
+    # header + 4 floats per row + per 32-row tile 2 x round_up(D, 16) floats
+    assert sc.scalify_layernorm_bwd_workspace_size(16384, 4096) == 256 + 4 * (4 * 16384 + 512 * 2 * 4096)
+    assert sc.scalify_layernorm_bwd_workspace_size(33, 17) == 256 + 4 * (4 * 33 + 2 * 2 * 32)
+    assert sc.scalify_layernorm_bwd_workspace_size(0, 16) == 256 + 4 * (1 * 2 * 16)
+    assert sc.scalify_layernorm_bwd_workspace_size(10, 8193) == 0
+
+
+@pytest.mark.parametrize("case,status", [
+    ("d_too_big", 3), ("d_zero", 3), ("out_f32", 2), ("shape", 3), ("trans", 4), ("ld_small", 3),
+    ("ld_unaligned", 5), ("gamma_unaligned", 5), ("eps_negative", 7), ("eps_nan", 7),
+    ("null_scale", 1), ("overlap", 4),
+])
+def test_layernorm_fwd_argument_errors(case, status):
+    x, out = arr(8, 64, dtype=sc.F16, ld=64), arr(8, 64, ld=64, data=FAKE + (1 << 20))
+    kw = {}
+    if case == "d_too_big":
+        x, out = arr(8, 8200, dtype=sc.F16, ld=8200), arr(8, 8200, ld=8208, data=FAKE + (1 << 20))
+    elif case == "d_zero":
+        x, out = arr(8, 0, dtype=sc.F16, ld=16), arr(8, 0, ld=16, data=FAKE + (1 << 20))
+    elif case == "out_f32":
+        out = arr(8, 64, dtype=sc.F32, ld=64, data=FAKE + (1 << 20))
+    elif case == "shape":
+        out = arr(8, 63, ld=64, data=FAKE + (1 << 20))
+    elif case == "trans":
+        x = arr(8, 64, dtype=sc.F16, ld=8, trans=1)
+    elif case == "ld_small":
+        x = arr(8, 64, dtype=sc.F16, ld=56)
+    elif case == "ld_unaligned":
+        x = arr(8, 64, dtype=sc.F16, ld=68)
+    elif case == "gamma_unaligned":
+        kw["gamma"] = FAKE + (2 << 20) + 4
+    elif case == "eps_negative":
+        kw["eps"] = -1.0
+    elif case == "eps_nan":
+        kw["eps"] = float("nan")
+    elif case == "null_scale":
+        out = arr(8, 64, ld=64, data=FAKE + (1 << 20), scale=None)
+    elif case == "overlap":
+        out = arr(8, 64, ld=64, data=FAKE + 64)
+    assert _ln_fwd(x, out, **kw) == status
+
+
+@pytest.mark.parametrize("case,status", [
+    ("mode", 7), ("shape_dy", 3), ("dx_f32", 2), ("ws_small", 6), ("ws_null", 6),
+    ("dgamma_unaligned", 5), ("dx_overlaps_x", 4),
+])
+def test_layernorm_bwd_argument_errors(case, status):
+    dy = arr(8, 64, dtype=sc.E5M2, ld=64)
+    x = arr(8, 64, dtype=sc.F16, ld=64, data=FAKE + (1 << 20))
+    dx = arr(8, 64, dtype=sc.E5M2, ld=64, data=FAKE + (2 << 20))
+    kw = {}
+    if case == "mode":
+        kw["mode"] = sc.RESCALE_DELAYED
+    elif case == "shape_dy":
+        dy = arr(9, 64, dtype=sc.E5M2, ld=64)
+    elif case == "dx_f32":
+        dx = arr(8, 64, dtype=sc.F32, ld=64, data=FAKE + (2 << 20))
+    elif case == "ws_small":
+        kw["ws_bytes"] = 256
+    elif case == "ws_null":
+        kw["ws"] = None
+    elif case == "dgamma_unaligned":
+        kw["dgamma"] = FAKE + (3 << 20) + 8
+    elif case == "dx_overlaps_x":
+        dx = arr(8, 64, dtype=sc.E5M2, ld=64, data=FAKE + (1 << 20) + 128)
+    assert _ln_bwd(dy, x, dx, **kw) == status
