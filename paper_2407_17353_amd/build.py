@@ -3,12 +3,20 @@
 Every .hip source under csrc/ is compiled by hipcc in parallel and linked into
 one shared library next to this file. Packed-fp32 instructions are disabled
 for all device code.
+
+The one-wave-per-SIMD GEMM kernels keep their accumulators in AGPRs that only
+their inline asm names (AccTile in csrc/gemm_kernel.h); the compiler does not
+know these registers hold values. The build therefore disassembles the GEMM
+objects and fails if, in any kernel that uses those accumulators, the
+compiler placed values of its own in AGPRs (an AGPR written from a VGPR or
+moved, which is how it spills) or used scratch memory.
 """
 from __future__ import annotations
 
 import concurrent.futures as cf
 import glob
 import os
+import re
 import subprocess
 import tempfile
 
@@ -29,6 +37,49 @@ def _hipcc() -> str:
     return os.path.join(rocm, "bin", "hipcc")
 
 
+def _llvm(tool: str) -> str:
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    return os.path.join(rocm, "llvm", "bin", tool)
+
+
+_KERNEL = re.compile(r"^[0-9a-f]+ <(\S+)>:$")
+_AGPR_MFMA = re.compile(r"v_mfma\S* a\[")
+_COMPILER_AGPR = re.compile(r"v_accvgpr_write_b32 a\d+, v\d+|v_accvgpr_mov_b32|scratch_")
+
+
+def check_accumulator_isolation(obj: str, tmp: str) -> int:
+    """Disassemble the gfx950 code of one object and check every kernel that
+    keeps accumulators in asm-named AGPRs. Returns the number of such
+    kernels; raises RuntimeError on a violation."""
+    base = os.path.join(tmp, os.path.basename(obj))
+    subprocess.run([_llvm("llvm-objcopy"), f"--dump-section=.hip_fatbin={base}.fatbin", obj],
+                   check=True, capture_output=True)
+    subprocess.run([_llvm("clang-offload-bundler"), "--unbundle", "--type=o",
+                    f"--input={base}.fatbin", f"--targets=hipv4-amdgcn-amd-amdhsa--{ARCH}",
+                    f"--output={base}.co"], check=True, capture_output=True)
+    dis = subprocess.run([_llvm("llvm-objdump"), "-d", f"--mcpu={ARCH}", f"{base}.co"],
+                         check=True, capture_output=True, text=True).stdout
+    kernels = {}
+    name = None
+    for line in dis.splitlines():
+        m = _KERNEL.match(line)
+        if m:
+            name = m.group(1)
+            kernels[name] = []
+        elif name is not None:
+            kernels[name].append(line)
+    checked = 0
+    for name, body in kernels.items():
+        if not any(_AGPR_MFMA.search(l) for l in body):
+            continue
+        checked += 1
+        bad = [l.strip() for l in body if _COMPILER_AGPR.search(l)]
+        if bad:
+            raise RuntimeError(f"{obj}: kernel {name} has compiler-placed AGPR or scratch "
+                               f"accesses next to the asm-held accumulators: {bad[:4]}")
+    return checked
+
+
 def build(verbose: bool = False) -> str:
     """Compile the library (always recompiles). Returns its path."""
     sources = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
@@ -41,6 +92,8 @@ def build(verbose: bool = False) -> str:
                 raise RuntimeError(f"hipcc failed for {src}:\n{r.stderr}")
             if verbose and r.stderr.strip():
                 print(r.stderr)
+            if os.path.basename(src).startswith("gemm_"):
+                check_accumulator_isolation(obj, tmp)
             return obj
 
         workers = min(len(sources), max(1, os.cpu_count() or 1), 8)

@@ -7,25 +7,30 @@
 // whole output) or, for the delayed rescale, whose output scale is known
 // before the GEMM starts, the output codes themselves.
 //
-// Design (per workgroup of 512 threads = 8 wave64, two per SIMD):
-//   * 256 x 256 output tile, K consumed in 128-byte steps; each wave owns a
-//     64 x 128 sub-tile = 4 x 8 tiles of v_mfma_f32_16x16x128_f8f6f4 with
-//     the accumulators in registers; the two waves of a SIMD cover each
-//     other's waits.
+// Design (per workgroup: one 256 x 256 output tile, K consumed in 128-byte
+// steps, v_mfma_f32_16x16x128_f8f6f4 tiles):
+//   * Two wave arrangements (WaveCfg): 4 waves, one per SIMD, each a
+//     128 x 128 sub-tile with its 256 accumulators pinned in AGPRs
+//     (AccTile), for the plain GEMM whose epilogue stores the pre-cast
+//     intermediate; 8 waves, two per SIMD, each a 64 x 128 sub-tile with
+//     the accumulators in VGPRs, for the epilogues that convert every value
+//     (direct cast, fused add / activation), where the second wave of a
+//     SIMD overlaps the first one's arithmetic and stores.
 //   * A and B k-slices (32 KiB each per step) stream HBM -> LDS with
 //     buffer_load_dwordx4 ... lds (16 B per lane, no VGPR staging) into two
 //     64 KiB stages. Buffer loads are range-checked: rows past the matrix,
 //     and K past its end, read as zeros without touching memory.
-//   * B fragments are read from LDS two column groups (8 MFMAs of the wave)
-//     ahead of their use.
-//   * Software pipeline with one barrier per step, placed before the last
-//     quarter of the step's MFMAs: by then every wave holds the B fragments
-//     it still needs, so after the barrier the step's stage is free and
-//     the loads of step s + 2 are issued into it, two per row block of
-//     MFMAs; in the same stretch each wave refills its A fragments with
-//     those of step s + 1 (landed before the barrier) as soon as their last
-//     MFMA has issued. MFMAs never wait for a barrier-to-first-fragment
-//     round trip, and loads have a whole step to land.
+//   * 8 waves: B fragments read from LDS two column groups ahead of their
+//     use; one barrier per step, placed before the last quarter of the
+//     step's MFMAs: by then every wave holds the B fragments it still
+//     needs, so after the barrier the step's stage is free and the loads of
+//     step s + 2 are issued into it, two per row block of MFMAs; in the same
+//     stretch each wave refills its A fragments with those of step s + 1
+//     (landed before the barrier) as soon as their last MFMA has issued.
+//   * 4 waves: every B fragment of a step in registers of its own, two
+//     barriers per step so that the A and B loads of step s + 2 spread over
+//     most of the step (a burst of loads fills the texture address path and
+//     stalls the only wave of the SIMD); see the schedule in gemm_kernel.
 //   * Operands whose K is contiguous in memory ("KC" tiles, 128 B rows) are
 //     read with ds_read_b128; operands whose M or N is contiguous ("MC"
 //     tiles, 256 B rows along k) are read with ds_read_b64_tr_b8, which
@@ -57,13 +62,24 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 #define LDS_AS __attribute__((address_space(3)))
 
 constexpr int BM = 256, BN = 256, BK = 128;
-// 8 waves (two per SIMD) arranged 4 x 2; each owns a 64 x 128 sub-tile.
-constexpr int WAVES = 8, WAVES_N = 2, WAVES_M = WAVES / WAVES_N, NTHR = 64 * WAVES;
-constexpr int WTM = BM / WAVES_M, WTN = BN / WAVES_N;      // 64 x 128
-constexpr int MI = WTM / 16, NI = WTN / 16;                // 4 x 8 MFMA tiles
-constexpr int BPW = 32 / WAVES;                            // 1 KiB load blocks per wave and operand
 constexpr int TILE_BYTES = 32768;
-constexpr int LOADS_PER_STEP = 2 * BPW;                    // load instructions per wave and step
+
+// Wave arrangement of a 256 x 256 tile, 2 waves along N:
+//   NW = 8: two waves per SIMD, each a 64 x 128 sub-tile (4 x 8 MFMA tiles,
+//           accumulators in 128 VGPRs); the two waves of a SIMD cover each
+//           other's waits.
+//   NW = 4: one wave per SIMD, each a 128 x 128 sub-tile (8 x 8 MFMA tiles,
+//           accumulators in 256 AGPRs): a third less LDS traffic per MFMA;
+//           every wait of the wave idles its SIMD's matrix core, so its
+//           fragments are read a step ahead (A double-buffered).
+template <int NW>
+struct WaveCfg {
+  static constexpr int WAVES = NW, WAVES_N = 2, WAVES_M = NW / 2, NTHR = 64 * NW;
+  static constexpr int WTM = BM / WAVES_M, WTN = BN / WAVES_N;
+  static constexpr int MI = WTM / 16, NI = WTN / 16;
+  static constexpr int BPW = 32 / NW;                // 1 KiB load blocks per wave and operand
+  static constexpr int LOADS_PER_STEP = 2 * BPW;     // load instructions per wave and step
+};
 
 // 16-byte chunk swizzles (see file comment). KC: 16 consecutive rows read
 // the same logical chunk from 16 distinct bank groups. MC: the 8 rows a
@@ -112,6 +128,14 @@ __device__ __forceinline__ void wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
+// Wait until at most N of this wave's LDS instructions are outstanding
+// (they complete in issue order).
+template <int N>
+__device__ __forceinline__ void wait_lgkmcnt() {
+  static_assert(N >= 0 && N < 16, "lgkmcnt range");
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory");
+}
+
 // Per-thread parts of the chunk offsets of one operand tile. Lane i of a
 // wave writes LDS bytes [16 i, 16 i + 16) of its 1 KiB block, so the
 // swizzle is applied to the global address; it depends on the lane and on
@@ -125,7 +149,7 @@ struct TileLoader {
   int kchunk[2];         // KC: k offset (bytes) of the lane's chunk, per parity
 };
 
-template <bool KC>
+template <bool KC, int BPW>
 __device__ __forceinline__ TileLoader make_loader(uint32_t ld, int wave, int lane) {
   TileLoader L;
   const int hi = ((wave * BPW) >> 3) & 1;  // bit 5 of the k-rows this wave loads (MC)
@@ -150,7 +174,7 @@ __device__ __forceinline__ TileLoader make_loader(uint32_t ld, int wave, int lan
 // through the buffer range check; KC chunks that start at or beyond K are
 // sent out of range too, and a chunk straddling K is trimmed by
 // zero_tail_kc.
-template <bool KC>
+template <bool KC, int BPW>
 __device__ __forceinline__ void issue_block(v4i rsrc, const TileLoader& L, uint32_t ld, int row0,
                                             int k0, int K, uint8_t* lds, int wave, int q) {
   const int blk = wave * BPW + q;
@@ -207,6 +231,148 @@ __device__ __forceinline__ v4f mfma(const v8i& bfrag, const v8i& afrag, const v4
   // First operand = B fragment (rows of the MFMA result index N), second =
   // A fragment: result lane l holds C[m = l & 15][n = 4 * (l >> 4) + i].
   return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(bfrag, afrag, c, FB, FA, 0, 0, 0, 0);
+}
+
+// One LDS read S of a fragment (read_frag split into its instructions, so
+// that they can be interleaved one by one with MFMAs): KC parts 0, 1 are
+// the two 16-byte halves, MC parts 0 .. 3 the four transposing reads.
+template <bool KC, int S>
+__device__ __forceinline__ void read_frag_part(v8i& f, const uint8_t* lds, int base, int lane) {
+  if constexpr (KC) {
+    const int r = base + (lane & 15);
+    const int g = lane >> 4;
+    const v4i h = *(const v4i*)(lds + r * 128 + (((2 * g + S) ^ swz_kc(r)) * 16));
+    f[4 * S + 0] = h.x;
+    f[4 * S + 1] = h.y;
+    f[4 * S + 2] = h.z;
+    f[4 * S + 3] = h.w;
+  } else {
+    const int t = lane & 15, g = lane >> 4;
+    const int k = 32 * g + 8 * S + (t >> 1);
+    const int off = k * 256 + (((base >> 4) ^ swz_mc(k)) * 16) + (t & 1) * 8;
+    const v2i v = __builtin_amdgcn_ds_read_tr8_b64_v2i32((LDS_AS v2i*)(lds + off));
+    f[2 * S] = v.x;
+    f[2 * S + 1] = v.y;
+  }
+}
+
+// Accumulators of the one-wave-per-SIMD GEMM: tile t (t = 8 mi + ni) of a
+// wave's 128 x 128 sub-tile lives in AGPRs a[4t .. 4t + 3] for the whole
+// main loop, named explicitly in inline asm, so that the compiler, which
+// otherwise rotates 256 accumulators through copies and spills, never holds
+// or moves them. Every statement declares the AGPRs it writes as clobbered;
+// the compiler allocates no AGPR of its own in these kernels (checked on
+// the built code object), so nothing else touches them. The compiler does
+// not see these MFMAs: their results are read only after mfma_drain().
+#define SCALIFY_ACC_TILES(X) \
+  X(0, "0:3", "0", "1", "2", "3") \
+  X(1, "4:7", "4", "5", "6", "7") \
+  X(2, "8:11", "8", "9", "10", "11") \
+  X(3, "12:15", "12", "13", "14", "15") \
+  X(4, "16:19", "16", "17", "18", "19") \
+  X(5, "20:23", "20", "21", "22", "23") \
+  X(6, "24:27", "24", "25", "26", "27") \
+  X(7, "28:31", "28", "29", "30", "31") \
+  X(8, "32:35", "32", "33", "34", "35") \
+  X(9, "36:39", "36", "37", "38", "39") \
+  X(10, "40:43", "40", "41", "42", "43") \
+  X(11, "44:47", "44", "45", "46", "47") \
+  X(12, "48:51", "48", "49", "50", "51") \
+  X(13, "52:55", "52", "53", "54", "55") \
+  X(14, "56:59", "56", "57", "58", "59") \
+  X(15, "60:63", "60", "61", "62", "63") \
+  X(16, "64:67", "64", "65", "66", "67") \
+  X(17, "68:71", "68", "69", "70", "71") \
+  X(18, "72:75", "72", "73", "74", "75") \
+  X(19, "76:79", "76", "77", "78", "79") \
+  X(20, "80:83", "80", "81", "82", "83") \
+  X(21, "84:87", "84", "85", "86", "87") \
+  X(22, "88:91", "88", "89", "90", "91") \
+  X(23, "92:95", "92", "93", "94", "95") \
+  X(24, "96:99", "96", "97", "98", "99") \
+  X(25, "100:103", "100", "101", "102", "103") \
+  X(26, "104:107", "104", "105", "106", "107") \
+  X(27, "108:111", "108", "109", "110", "111") \
+  X(28, "112:115", "112", "113", "114", "115") \
+  X(29, "116:119", "116", "117", "118", "119") \
+  X(30, "120:123", "120", "121", "122", "123") \
+  X(31, "124:127", "124", "125", "126", "127") \
+  X(32, "128:131", "128", "129", "130", "131") \
+  X(33, "132:135", "132", "133", "134", "135") \
+  X(34, "136:139", "136", "137", "138", "139") \
+  X(35, "140:143", "140", "141", "142", "143") \
+  X(36, "144:147", "144", "145", "146", "147") \
+  X(37, "148:151", "148", "149", "150", "151") \
+  X(38, "152:155", "152", "153", "154", "155") \
+  X(39, "156:159", "156", "157", "158", "159") \
+  X(40, "160:163", "160", "161", "162", "163") \
+  X(41, "164:167", "164", "165", "166", "167") \
+  X(42, "168:171", "168", "169", "170", "171") \
+  X(43, "172:175", "172", "173", "174", "175") \
+  X(44, "176:179", "176", "177", "178", "179") \
+  X(45, "180:183", "180", "181", "182", "183") \
+  X(46, "184:187", "184", "185", "186", "187") \
+  X(47, "188:191", "188", "189", "190", "191") \
+  X(48, "192:195", "192", "193", "194", "195") \
+  X(49, "196:199", "196", "197", "198", "199") \
+  X(50, "200:203", "200", "201", "202", "203") \
+  X(51, "204:207", "204", "205", "206", "207") \
+  X(52, "208:211", "208", "209", "210", "211") \
+  X(53, "212:215", "212", "213", "214", "215") \
+  X(54, "216:219", "216", "217", "218", "219") \
+  X(55, "220:223", "220", "221", "222", "223") \
+  X(56, "224:227", "224", "225", "226", "227") \
+  X(57, "228:231", "228", "229", "230", "231") \
+  X(58, "232:235", "232", "233", "234", "235") \
+  X(59, "236:239", "236", "237", "238", "239") \
+  X(60, "240:243", "240", "241", "242", "243") \
+  X(61, "244:247", "244", "245", "246", "247") \
+  X(62, "248:251", "248", "249", "250", "251") \
+  X(63, "252:255", "252", "253", "254", "255")
+
+template <int T>
+struct AccTile;
+
+// cbsz / blgp select the FP8 formats of the first (B fragment) / second (A
+// fragment) operand: 0 E4M3, 1 E5M2.
+#define SCALIFY_ACC_TILE(t, r, r0, r1, r2, r3)                                                  \
+  template <>                                                                                  \
+  struct AccTile<t> {                                                                          \
+    template <int FA, int FB>                                                                  \
+    static __device__ __forceinline__ void mfma(const v8i& b, const v8i& a) {                  \
+      if constexpr (FB == 0 && FA == 0)                                                        \
+        asm volatile("v_mfma_f32_16x16x128_f8f6f4 a[" r "], %0, %1, a[" r "]"                  \
+                     :: "v"(b), "v"(a) : "a" r0, "a" r1, "a" r2, "a" r3);                      \
+      else if constexpr (FB == 1 && FA == 0)                                                   \
+        asm volatile("v_mfma_f32_16x16x128_f8f6f4 a[" r "], %0, %1, a[" r "] cbsz:1"           \
+                     :: "v"(b), "v"(a) : "a" r0, "a" r1, "a" r2, "a" r3);                      \
+      else if constexpr (FB == 0 && FA == 1)                                                   \
+        asm volatile("v_mfma_f32_16x16x128_f8f6f4 a[" r "], %0, %1, a[" r "] blgp:1"           \
+                     :: "v"(b), "v"(a) : "a" r0, "a" r1, "a" r2, "a" r3);                      \
+      else                                                                                     \
+        asm volatile("v_mfma_f32_16x16x128_f8f6f4 a[" r "], %0, %1, a[" r "] cbsz:1 blgp:1"    \
+                     :: "v"(b), "v"(a) : "a" r0, "a" r1, "a" r2, "a" r3);                      \
+    }                                                                                          \
+    static __device__ __forceinline__ void zero() {                                            \
+      asm volatile("v_accvgpr_write_b32 a" r0 ", 0\n\tv_accvgpr_write_b32 a" r1 ", 0\n\t"       \
+                   "v_accvgpr_write_b32 a" r2 ", 0\n\tv_accvgpr_write_b32 a" r3 ", 0"          \
+                   ::: "a" r0, "a" r1, "a" r2, "a" r3);                                        \
+    }                                                                                          \
+    static __device__ __forceinline__ v4f read() {                                             \
+      float x0, x1, x2, x3;                                                                    \
+      asm volatile("v_accvgpr_read_b32 %0, a" r0 "\n\tv_accvgpr_read_b32 %1, a" r1 "\n\t"      \
+                   "v_accvgpr_read_b32 %2, a" r2 "\n\tv_accvgpr_read_b32 %3, a" r3               \
+                   : "=v"(x0), "=v"(x1), "=v"(x2), "=v"(x3));                                  \
+      return v4f{x0, x1, x2, x3};                                                              \
+    }                                                                                          \
+  };
+SCALIFY_ACC_TILES(SCALIFY_ACC_TILE)
+#undef SCALIFY_ACC_TILE
+
+// Wait states after the last AccTile write before its registers are read by
+// other instructions (more than the 8-pass MFMA's result latency).
+__device__ __forceinline__ void mfma_drain() {
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
 }
 
 template <int I, int N, typename F>
@@ -386,8 +552,12 @@ __device__ __forceinline__ void activate(v4f (&acc)[MI_][NI_], int e_w) {
   });
 }
 
-template <bool A_MN, bool B_KC, int FA, int FB, int EPI, bool FUSE>
-__global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
+template <bool A_MN, bool B_KC, int FA, int FB, int EPI, bool FUSE, int NW>
+__global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
+  static_assert(NW == 8 || (NW == 4 && !FUSE), "the fused epilogue runs on the 8-wave kernel");
+  using C = WaveCfg<NW>;
+  constexpr int WAVES = C::WAVES, WAVES_N = C::WAVES_N, WTM = C::WTM, WTN = C::WTN;
+  constexpr int MI = C::MI, NI = C::NI, BPW = C::BPW, LOADS_PER_STEP = C::LOADS_PER_STEP;
   __shared__ __attribute__((aligned(1024))) uint8_t sA0[TILE_BYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t sB0[TILE_BYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t sA1[TILE_BYTES];
@@ -420,15 +590,15 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
   // B: KC when stored [N][K], MC when stored [K][N].
   const v4i ra = make_rsrc(p.a, p.a_bytes);
   const v4i rb = make_rsrc(p.b, p.b_bytes);
-  const TileLoader la = make_loader<!A_MN>(lda, wave, lane);
-  const TileLoader lb = make_loader<B_KC>(ldb, wave, lane);
+  const TileLoader la = make_loader<!A_MN, BPW>(lda, wave, lane);
+  const TileLoader lb = make_loader<B_KC, BPW>(ldb, wave, lane);
 
   // Load j of a step: j < BPW are A blocks, the rest B blocks.
   auto issue_one = [&](int j, int kt, uint8_t* dA, uint8_t* dB) {
     if (j < BPW)
-      issue_block<!A_MN>(ra, la, lda, m0, kt * BK, K, dA, wave, j);
+      issue_block<!A_MN, BPW>(ra, la, lda, m0, kt * BK, K, dA, wave, j);
     else
-      issue_block<B_KC>(rb, lb, ldb, n0, kt * BK, K, dB, wave, j - BPW);
+      issue_block<B_KC, BPW>(rb, lb, ldb, n0, kt * BK, K, dB, wave, j - BPW);
   };
   auto issue_all = [&](int kt, uint8_t* dA, uint8_t* dB) {
 #pragma unroll
@@ -441,100 +611,229 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
     __syncthreads();
   };
 
-  v4f acc[MI][NI];
+  v4f acc[MI][NI];  // NW = 8 (NW = 4: AccTile)
+  if constexpr (NW == 8) {
 #pragma unroll
-  for (int i = 0; i < MI; ++i)
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
-    for (int j = 0; j < NI; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+      for (int j = 0; j < NI; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+  } else {
+    static_for<0, MI * NI>([&](auto I) { AccTile<decltype(I)::value>::zero(); });
+    mfma_drain();
+  }
 
   const int wm = (wave / WAVES_N) * WTM;  // wave sub-tile
   const int wn = (wave % WAVES_N) * WTN;
   constexpr int DSA = A_MN ? 4 : 2;  // LDS reads per A fragment
   constexpr int DSB = B_KC ? 2 : 4;  // LDS reads per B fragment
-
-  v8i a[MI];   // A fragments of the step
-  v8i bq[3];   // B fragments: in use and up to two groups ahead
-
-  // One k-step. LOADS: issue the loads of step kt + 2 into this step's
-  // stage after the barrier. NEXT: step kt + 1 exists (barrier, then its A
-  // fragments and first B fragment are read into a[] and b).
-  auto step = [&](auto loads_tag, auto next_tag, int kt) {
-    constexpr bool LOADS = decltype(loads_tag)::value;
-    constexpr bool NEXT = decltype(next_tag)::value;
-    const bool odd = kt & 1;
-    uint8_t* cA = odd ? sA1 : sA0;  // this step's stage
-    uint8_t* cB = odd ? sB1 : sB0;
-    uint8_t* nA = odd ? sA0 : sA1;  // the next step's stage
-    uint8_t* nB = odd ? sB0 : sB1;
-    // B column groups 0 .. NI - 3, fragments read two groups ahead
-    static_for<0, NI - 2>([&](auto I) {
-      constexpr int ni = decltype(I)::value;
-      bq[(ni + 2) % 3] = read_frag<B_KC>(cB, wn + 16 * (ni + 2), lane);
-#pragma unroll
-      for (int mi = 0; mi < MI; ++mi) acc[mi][ni] = mfma<FA, FB>(bq[ni % 3], a[mi], acc[mi][ni]);
-#pragma unroll
-      for (int mi = 0; mi < MI; ++mi) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        if (mi < DSB) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      }
-    });
-    if (NEXT) {
-      // Every wave holds all B fragments of this step once its LDS reads
-      // have returned (the barrier waits for them), so this stage is free
-      // after the barrier; step kt + 1 has landed once every wave's loads
-      // have completed.
-      wait_vmcnt<0>();
-      __builtin_amdgcn_sched_barrier(0);
-      __syncthreads();
-      __builtin_amdgcn_sched_barrier(0);
-      if (!LOADS && kt + 1 == KT_full && (krem & 15)) zero_tail(nA, nB);
-    }
-    // B column groups NI - 2 and NI - 1, taken row block by row block: once
-    // both MFMAs of a[mi] have issued, a[mi] is refilled with the fragment
-    // of step kt + 1; the loads of step kt + 2 go out two per row block.
-    static_assert(LOADS_PER_STEP == 2 * MI, "two loads per row block");
-#pragma unroll
-    for (int mi = 0; mi < MI; ++mi) {
-      acc[mi][NI - 2] = mfma<FA, FB>(bq[(NI - 2) % 3], a[mi], acc[mi][NI - 2]);
-      acc[mi][NI - 1] = mfma<FA, FB>(bq[(NI - 1) % 3], a[mi], acc[mi][NI - 1]);
-      if (LOADS) {
-        issue_one(2 * mi, kt + 2, cA, cB);
-        issue_one(2 * mi + 1, kt + 2, cA, cB);
-      }
-      if (NEXT) a[mi] = read_frag<!A_MN>(nA, wm + 16 * mi, lane);
-    }
-    if (NEXT) {
-      bq[0] = read_frag<B_KC>(nB, wn, lane);
-      bq[1] = read_frag<B_KC>(nB, wn + 16, lane);
-    }
-    static_for<0, MI>([&](auto I) {
-      constexpr int i = decltype(I)::value;
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-      if (NEXT) __builtin_amdgcn_sched_group_barrier(0x100, i + 1 < MI ? DSA : DSA + 2 * DSB, 0);
-    });
-  };
-
-  if (KT > 0) {
-    issue_all(0, sA0, sB0);
-    if (KT > 1) {
-      issue_all(1, sA1, sB1);
-      wait_vmcnt<LOADS_PER_STEP>();
-    } else {
-      wait_vmcnt<0>();
-    }
-    __syncthreads();
-    if (KT_full == 0 && (krem & 15)) zero_tail(sA0, sB0);
-#pragma unroll
-    for (int mi = 0; mi < MI; ++mi) a[mi] = read_frag<!A_MN>(sA0, wm + 16 * mi, lane);
-    bq[0] = read_frag<B_KC>(sB0, wn, lane);
-    bq[1] = read_frag<B_KC>(sB0, wn + 16, lane);
-  }
+  static_assert(LOADS_PER_STEP == 2 * MI, "two loads per row block");
   using T_ = std::true_type;
   using F_ = std::false_type;
-  int kt = 0;
-  for (; kt + 2 < KT; ++kt) step(T_{}, T_{}, kt);
-  if (kt + 1 < KT) step(F_{}, T_{}, kt++);
-  if (kt < KT) step(F_{}, F_{}, kt);
+
+  if constexpr (NW == 8) {
+    v8i a[MI];   // A fragments of the step
+    v8i bq[3];   // B fragments: in use and up to two groups ahead
+
+    // One k-step. LOADS: issue the loads of step kt + 2 into this step's
+    // stage after the barrier. NEXT: step kt + 1 exists (barrier, then its A
+    // fragments and first B fragment are read into a[] and b).
+    auto step = [&](auto loads_tag, auto next_tag, int kt) {
+      constexpr bool LOADS = decltype(loads_tag)::value;
+      constexpr bool NEXT = decltype(next_tag)::value;
+      const bool odd = kt & 1;
+      uint8_t* cA = odd ? sA1 : sA0;  // this step's stage
+      uint8_t* cB = odd ? sB1 : sB0;
+      uint8_t* nA = odd ? sA0 : sA1;  // the next step's stage
+      uint8_t* nB = odd ? sB0 : sB1;
+      // B column groups 0 .. NI - 3, fragments read two groups ahead
+      static_for<0, NI - 2>([&](auto I) {
+        constexpr int ni = decltype(I)::value;
+        bq[(ni + 2) % 3] = read_frag<B_KC>(cB, wn + 16 * (ni + 2), lane);
+#pragma unroll
+        for (int mi = 0; mi < MI; ++mi) acc[mi][ni] = mfma<FA, FB>(bq[ni % 3], a[mi], acc[mi][ni]);
+#pragma unroll
+        for (int mi = 0; mi < MI; ++mi) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          if (mi < DSB) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+      });
+      if (NEXT) {
+        // Every wave holds all B fragments of this step once its LDS reads
+        // have returned (the barrier waits for them), so this stage is free
+        // after the barrier; step kt + 1 has landed once every wave's loads
+        // have completed.
+        wait_vmcnt<0>();
+        __builtin_amdgcn_sched_barrier(0);
+        __syncthreads();
+        __builtin_amdgcn_sched_barrier(0);
+        if (!LOADS && kt + 1 == KT_full && (krem & 15)) zero_tail(nA, nB);
+      }
+      // B column groups NI - 2 and NI - 1, taken row block by row block: once
+      // both MFMAs of a[mi] have issued, a[mi] is refilled with the fragment
+      // of step kt + 1; the loads of step kt + 2 go out two per row block.
+#pragma unroll
+      for (int mi = 0; mi < MI; ++mi) {
+        acc[mi][NI - 2] = mfma<FA, FB>(bq[(NI - 2) % 3], a[mi], acc[mi][NI - 2]);
+        acc[mi][NI - 1] = mfma<FA, FB>(bq[(NI - 1) % 3], a[mi], acc[mi][NI - 1]);
+        if (LOADS) {
+          issue_one(2 * mi, kt + 2, cA, cB);
+          issue_one(2 * mi + 1, kt + 2, cA, cB);
+        }
+        if (NEXT) a[mi] = read_frag<!A_MN>(nA, wm + 16 * mi, lane);
+      }
+      if (NEXT) {
+        bq[0] = read_frag<B_KC>(nB, wn, lane);
+        bq[1] = read_frag<B_KC>(nB, wn + 16, lane);
+      }
+      static_for<0, MI>([&](auto I) {
+        constexpr int i = decltype(I)::value;
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        if (NEXT) __builtin_amdgcn_sched_group_barrier(0x100, i + 1 < MI ? DSA : DSA + 2 * DSB, 0);
+      });
+    };
+
+    if (KT > 0) {
+      issue_all(0, sA0, sB0);
+      if (KT > 1) {
+        issue_all(1, sA1, sB1);
+        wait_vmcnt<LOADS_PER_STEP>();
+      } else {
+        wait_vmcnt<0>();
+      }
+      __syncthreads();
+      if (KT_full == 0 && (krem & 15)) zero_tail(sA0, sB0);
+#pragma unroll
+      for (int mi = 0; mi < MI; ++mi) a[mi] = read_frag<!A_MN>(sA0, wm + 16 * mi, lane);
+      bq[0] = read_frag<B_KC>(sB0, wn, lane);
+      bq[1] = read_frag<B_KC>(sB0, wn + 16, lane);
+    }
+    int kt = 0;
+    for (; kt + 2 < KT; ++kt) step(T_{}, T_{}, kt);
+    if (kt + 1 < KT) step(F_{}, T_{}, kt++);
+    if (kt < KT) step(F_{}, F_{}, kt);
+  } else {
+    // One wave per SIMD: every B fragment of a step in a register buffer of
+    // its own (bf[ni] for column group ni); A fragments refilled row block
+    // by row block once their last MFMA of the step has issued. Two
+    // barriers per step spread the step's 16 loads over most of it (the
+    // texture address path accepts about one 1 KiB load per 16 cycles per
+    // CU, so loads issued in a burst stall the wave's instruction stream
+    // and with it the matrix core):
+    //   head(kt), column groups 0 .. H - 1, which also reads the B
+    //     fragments of groups 2 .. NI - 1, one LDS read after each MFMA;
+    //     barrier X after group 0 (every wave has read step kt's A
+    //     fragments, in the previous tail), then the A loads of step kt + 2
+    //     into this step's A stage, spread over groups 1 .. H - 1;
+    //     barrier Y at its end (every wave has read step kt's B fragments,
+    //     and step kt + 1 has landed: only the A loads of step kt + 2 may
+    //     still be in flight);
+    //   tail(kt), groups H .. NI - 1 row block by row block, with the B
+    //     loads of step kt + 2 into this step's B stage, the refill of each
+    //     A fragment with step kt + 1's after its last MFMA, and the reads
+    //     of step kt + 1's B fragments 0 and 1.
+    // The loop runs tail(kt) + head(kt + 1). Every step has the same shape:
+    // loads of steps >= KT are range-checked to zeros and fragment reads of
+    // step KT are never used, which keeps one copy of the loop body.
+    // Program order is issue order (AccTile MFMAs are volatile asm), so the
+    // interleave is written out; the waits at the barriers are explicit
+    // (outstanding loads counted in issue order, which is also the order in
+    // which they complete).
+    constexpr int H = 6;
+    static_assert(H >= 3 && H < NI && (NI - 2) * DSB <= H * MI, "head too short for its B reads");
+    constexpr int TS = (NI - H) * MI;          // MFMAs of the tail
+    constexpr int AS = (H - 1) * MI;           // MFMAs of the head after barrier X
+    constexpr int BP = 2 * DSB;                // LDS reads of the next step's B fragments 0, 1
+    constexpr int RX = MI < (NI - 2) * DSB ? MI : (NI - 2) * DSB;  // B reads issued before X
+    v8i af[MI];
+    v8i bf[NI];
+
+    auto head = [&](int kt) {
+      const bool odd = kt & 1;
+      uint8_t* cA = odd ? sA1 : sA0;
+      uint8_t* cB = odd ? sB1 : sB0;
+      static_for<0, H * MI>([&](auto I) {
+        constexpr int i = decltype(I)::value;
+        constexpr int ni = i / MI, mi = i % MI;
+        AccTile<mi * NI + ni>::template mfma<FA, FB>(bf[ni], af[mi]);
+        if constexpr (i < (NI - 2) * DSB) {
+          constexpr int g = 2 + i / DSB;  // column group whose fragment part is read
+          read_frag_part<B_KC, i % DSB>(bf[g], cB, wn + 16 * g, lane);
+        }
+        if constexpr (i == MI - 1) {
+          // X: this wave's reads of step kt's A fragments (issued before
+          // the RX B reads of this head) are done; once all waves are, the
+          // A stage takes step kt + 2.
+          wait_lgkmcnt<RX>();
+          __builtin_amdgcn_s_barrier();
+        }
+        if constexpr (i >= MI) {
+          constexpr int j = i - MI;  // A loads [j * BPW / AS, (j + 1) * BPW / AS)
+          static_for<j * BPW / AS, (j + 1) * BPW / AS>([&](auto J) {
+            issue_one(decltype(J)::value, kt + 2, cA, cB);
+          });
+        }
+      });
+      // Y: step kt + 1 has landed (its A loads went out in the previous
+      // head, its B loads in the previous tail; only this head's BPW loads
+      // may be outstanding) and this wave's B reads of step kt are done.
+      wait_vmcnt<BPW>();
+      wait_lgkmcnt<0>();
+      __builtin_amdgcn_s_barrier();
+      if (kt + 1 == KT_full && (krem & 15)) zero_tail(odd ? sA0 : sA1, odd ? sB0 : sB1);
+    };
+    auto tail = [&](int kt) {
+      const bool odd = kt & 1;
+      uint8_t* cA = odd ? sA1 : sA0;  // this step's stage
+      uint8_t* cB = odd ? sB1 : sB0;
+      uint8_t* nA = odd ? sA0 : sA1;  // the next step's stage
+      uint8_t* nB = odd ? sB0 : sB1;
+      static_for<0, TS>([&](auto I) {
+        constexpr int i = decltype(I)::value;
+        constexpr int mi = i / (NI - H), ni = H + i % (NI - H);
+        AccTile<mi * NI + ni>::template mfma<FA, FB>(bf[ni], af[mi]);
+        // B loads [i * BPW / TS, (i + 1) * BPW / TS) of step kt + 2
+        static_for<i * BPW / TS, (i + 1) * BPW / TS>([&](auto J) {
+          issue_one(BPW + decltype(J)::value, kt + 2, cA, cB);
+        });
+        // reads [i * BP / TS, (i + 1) * BP / TS) of the next step's B fragments 0, 1
+        static_for<i * BP / TS, (i + 1) * BP / TS>([&](auto Q) {
+          constexpr int q = decltype(Q)::value;
+          read_frag_part<B_KC, q % DSB>(bf[q / DSB], nB, wn + 16 * (q / DSB), lane);
+        });
+        if constexpr (ni == NI - 1) {  // last MFMA of af[mi] in this step
+          static_for<0, DSA>([&](auto Q) {
+            read_frag_part<!A_MN, decltype(Q)::value>(af[mi], nA, wm + 16 * mi, lane);
+          });
+        }
+      });
+    };
+
+    if (KT > 0) {
+      issue_all(0, sA0, sB0);
+      issue_all(1, sA1, sB1);
+      wait_vmcnt<LOADS_PER_STEP>();
+      __syncthreads();
+      if (KT_full == 0 && (krem & 15)) zero_tail(sA0, sB0);
+#pragma unroll
+      for (int mi = 0; mi < MI; ++mi) af[mi] = read_frag<!A_MN>(sA0, wm + 16 * mi, lane);
+      bf[0] = read_frag<B_KC>(sB0, wn, lane);
+      bf[1] = read_frag<B_KC>(sB0, wn + 16, lane);
+      head(0);
+      // The last tail stays inside the loop, so that no copy of the
+      // accumulators can be placed between MFMAs; the drain precedes the
+      // exit, so that copies the compiler places on the exit edge read
+      // complete results.
+      for (int kt = 0;; ++kt) {
+        tail(kt);
+        if (kt + 1 >= KT) {
+          wait_vmcnt<0>();  // the (range-checked) loads of steps KT and KT + 1
+          mfma_drain();
+          break;
+        }
+        head(kt + 1);
+      }
+    }
+  }
 
   // ---- epilogue: lane holds C[m][n..n+3] for each (mi, ni)
   float lmax = 0.f;
@@ -585,7 +884,10 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
     const int m = mb + 16 * mi;
     const int n = nb + 16 * ni;
     if (m < M && n < N) {
-      const v4f v = acc[mi][ni];  // FUSE: w
+      // FUSE: w; one wave per SIMD: read from the tile's AGPRs
+      v4f v;
+      if constexpr (NW == 4) v = AccTile<decltype(I)::value>::read();
+      else v = acc[mi][ni];
       lmax = fmaxf(lmax, fabsf(v[0]));
       if (n + 1 < N) lmax = fmaxf(lmax, fabsf(v[1]));
       if (n + 2 < N) lmax = fmaxf(lmax, fabsf(v[2]));
@@ -640,7 +942,7 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
         }
       }
       if (!FUSE && p.acc_out) {
-        const v4f a = acc[mi][ni];
+        const v4f a = v;
         float* q = p.acc_out + (int64_t)m * N + n;
         q[0] = a[0];
         if (n + 1 < N) q[1] = a[1];
@@ -677,21 +979,31 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmParams p) {
 template <bool A_MN, bool B_KC, bool FUSE>
 hipError_t launch_layout(const GemmParams& p, int fa, int fb, int epi, hipStream_t s);
 
+// Wave arrangement per kernel: one wave per SIMD where the epilogue stores
+// the pre-cast intermediate (its main loop is the faster one); two waves
+// per SIMD where the epilogue converts every value itself (direct cast of
+// the delayed rescale, fused add / activation), whose arithmetic the second
+// wave of a SIMD overlaps with the first one's stores.
+constexpr int gemm_waves(int epi, bool fuse) { return (fuse || epi == EPI_DIRECT) ? 8 : 4; }
+
+template <bool A_MN, bool B_KC, bool FUSE, int FA, int FB, int EPI>
+hipError_t launch_epi(const GemmParams& p, hipStream_t s) {
+  constexpr int NW = gemm_waves(EPI, FUSE);
+  const dim3 grid(p.tiles_m * p.tiles_n), block(WaveCfg<NW>::NTHR);
+  hipLaunchKernelGGL((gemm_kernel<A_MN, B_KC, FA, FB, EPI, FUSE, NW>), grid, block, 0, s, p);
+  return hipGetLastError();
+}
+
 template <bool A_MN, bool B_KC, bool FUSE, int FA, int FB>
 hipError_t launch_fmt(const GemmParams& p, int epi, hipStream_t s) {
-  const dim3 grid(p.tiles_m * p.tiles_n), block(NTHR);
   switch (epi) {
     case EPI_INTER16:
-      hipLaunchKernelGGL((gemm_kernel<A_MN, B_KC, FA, FB, EPI_INTER16, FUSE>), grid, block, 0, s, p);
-      break;
+      return launch_epi<A_MN, B_KC, FUSE, FA, FB, EPI_INTER16>(p, s);
     case EPI_INTER32:
-      hipLaunchKernelGGL((gemm_kernel<A_MN, B_KC, FA, FB, EPI_INTER32, FUSE>), grid, block, 0, s, p);
-      break;
+      return launch_epi<A_MN, B_KC, FUSE, FA, FB, EPI_INTER32>(p, s);
     default:
-      hipLaunchKernelGGL((gemm_kernel<A_MN, B_KC, FA, FB, EPI_DIRECT, FUSE>), grid, block, 0, s, p);
-      break;
+      return launch_epi<A_MN, B_KC, FUSE, FA, FB, EPI_DIRECT>(p, s);
   }
-  return hipGetLastError();
 }
 
 template <bool A_MN, bool B_KC, bool FUSE>
