@@ -713,12 +713,11 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
     if (kt < KT) step(F_{}, F_{}, kt);
   } else {
     // One wave per SIMD: every B fragment of a step in a register buffer of
-    // its own (bf[ni] for column group ni); A fragments refilled row block
-    // by row block once their last MFMA of the step has issued. Two
-    // barriers per step spread the step's 16 loads over most of it (the
-    // texture address path accepts about one 1 KiB load per 16 cycles per
-    // CU, so loads issued in a burst stall the wave's instruction stream
-    // and with it the matrix core):
+    // its own (bf[ni] for column group ni), A fragments double-buffered by
+    // step parity (af[kt & 1]). Two barriers per step spread the step's 16
+    // loads over most of it (the texture address path accepts about one
+    // 1 KiB load per 16 cycles per CU, so loads issued in a burst stall the
+    // wave's instruction stream and with it the matrix core):
     //   head(kt), column groups 0 .. H - 1, which also reads the B
     //     fragments of groups 2 .. NI - 1, one LDS read after each MFMA;
     //     barrier X after group 0 (every wave has read step kt's A
@@ -728,33 +727,34 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
     //     and step kt + 1 has landed: only the A loads of step kt + 2 may
     //     still be in flight);
     //   tail(kt), groups H .. NI - 1 row block by row block, with the B
-    //     loads of step kt + 2 into this step's B stage, the refill of each
-    //     A fragment with step kt + 1's after its last MFMA, and the reads
-    //     of step kt + 1's B fragments 0 and 1.
-    // The loop runs tail(kt) + head(kt + 1). Every step has the same shape:
-    // loads of steps >= KT are range-checked to zeros and fragment reads of
-    // step KT are never used, which keeps one copy of the loop body.
-    // Program order is issue order (AccTile MFMAs are volatile asm), so the
-    // interleave is written out; the waits at the barriers are explicit
-    // (outstanding loads counted in issue order, which is also the order in
-    // which they complete).
+    //     loads of step kt + 2 into this step's B stage and the reads of
+    //     step kt + 1's A fragments (into the other buffer) and B fragments
+    //     0 and 1, all spread over its MFMAs.
+    // The loop runs tail(kt) + head(kt + 1), unrolled by two for the parity
+    // of the A buffers. Every step has the same shape: loads of steps >= KT
+    // are range-checked to zeros and fragment reads of step KT are never
+    // used, which keeps one copy of the loop body. Program order is issue
+    // order (AccTile MFMAs are volatile asm), so the interleave is written
+    // out; the waits at the barriers are explicit (outstanding loads counted
+    // in issue order, which is also the order in which they complete).
     constexpr int H = 6;
     static_assert(H >= 3 && H < NI && (NI - 2) * DSB <= H * MI, "head too short for its B reads");
     constexpr int TS = (NI - H) * MI;          // MFMAs of the tail
     constexpr int AS = (H - 1) * MI;           // MFMAs of the head after barrier X
     constexpr int BP = 2 * DSB;                // LDS reads of the next step's B fragments 0, 1
     constexpr int RX = MI < (NI - 2) * DSB ? MI : (NI - 2) * DSB;  // B reads issued before X
-    v8i af[MI];
+    v8i af[2][MI];
     v8i bf[NI];
 
-    auto head = [&](int kt) {
+    auto head = [&](auto par_tag, int kt) {
+      constexpr int P = decltype(par_tag)::value;
       const bool odd = kt & 1;
       uint8_t* cA = odd ? sA1 : sA0;
       uint8_t* cB = odd ? sB1 : sB0;
       static_for<0, H * MI>([&](auto I) {
         constexpr int i = decltype(I)::value;
         constexpr int ni = i / MI, mi = i % MI;
-        AccTile<mi * NI + ni>::template mfma<FA, FB>(bf[ni], af[mi]);
+        AccTile<mi * NI + ni>::template mfma<FA, FB>(bf[ni], af[P][mi]);
         if constexpr (i < (NI - 2) * DSB) {
           constexpr int g = 2 + i / DSB;  // column group whose fragment part is read
           read_frag_part<B_KC, i % DSB>(bf[g], cB, wn + 16 * g, lane);
@@ -781,7 +781,8 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
       __builtin_amdgcn_s_barrier();
       if (kt + 1 == KT_full && (krem & 15)) zero_tail(odd ? sA0 : sA1, odd ? sB0 : sB1);
     };
-    auto tail = [&](int kt) {
+    auto tail = [&](auto par_tag, int kt) {
+      constexpr int P = decltype(par_tag)::value;
       const bool odd = kt & 1;
       uint8_t* cA = odd ? sA1 : sA0;  // this step's stage
       uint8_t* cB = odd ? sB1 : sB0;
@@ -790,7 +791,7 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
       static_for<0, TS>([&](auto I) {
         constexpr int i = decltype(I)::value;
         constexpr int mi = i / (NI - H), ni = H + i % (NI - H);
-        AccTile<mi * NI + ni>::template mfma<FA, FB>(bf[ni], af[mi]);
+        AccTile<mi * NI + ni>::template mfma<FA, FB>(bf[ni], af[P][mi]);
         // B loads [i * BPW / TS, (i + 1) * BPW / TS) of step kt + 2
         static_for<i * BPW / TS, (i + 1) * BPW / TS>([&](auto J) {
           issue_one(BPW + decltype(J)::value, kt + 2, cA, cB);
@@ -800,11 +801,11 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
           constexpr int q = decltype(Q)::value;
           read_frag_part<B_KC, q % DSB>(bf[q / DSB], nB, wn + 16 * (q / DSB), lane);
         });
-        if constexpr (ni == NI - 1) {  // last MFMA of af[mi] in this step
-          static_for<0, DSA>([&](auto Q) {
-            read_frag_part<!A_MN, decltype(Q)::value>(af[mi], nA, wm + 16 * mi, lane);
-          });
-        }
+        // A reads [i * AR / TS, (i + 1) * AR / TS) of the next step, into the other buffer
+        static_for<i * (MI * DSA) / TS, (i + 1) * (MI * DSA) / TS>([&](auto Q) {
+          constexpr int q = decltype(Q)::value;
+          read_frag_part<!A_MN, q % DSA>(af[P ^ 1][q / DSA], nA, wm + 16 * (q / DSA), lane);
+        });
       });
     };
 
@@ -815,23 +816,22 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
       __syncthreads();
       if (KT_full == 0 && (krem & 15)) zero_tail(sA0, sB0);
 #pragma unroll
-      for (int mi = 0; mi < MI; ++mi) af[mi] = read_frag<!A_MN>(sA0, wm + 16 * mi, lane);
+      for (int mi = 0; mi < MI; ++mi) af[0][mi] = read_frag<!A_MN>(sA0, wm + 16 * mi, lane);
       bf[0] = read_frag<B_KC>(sB0, wn, lane);
       bf[1] = read_frag<B_KC>(sB0, wn + 16, lane);
-      head(0);
-      // The last tail stays inside the loop, so that no copy of the
-      // accumulators can be placed between MFMAs; the drain precedes the
-      // exit, so that copies the compiler places on the exit edge read
-      // complete results.
-      for (int kt = 0;; ++kt) {
-        tail(kt);
-        if (kt + 1 >= KT) {
-          wait_vmcnt<0>();  // the (range-checked) loads of steps KT and KT + 1
-          mfma_drain();
-          break;
-        }
-        head(kt + 1);
+      using P0 = std::integral_constant<int, 0>;
+      using P1 = std::integral_constant<int, 1>;
+      head(P0{}, 0);
+      for (int kt = 0;; kt += 2) {
+        tail(P0{}, kt);
+        if (kt + 1 >= KT) break;
+        head(P1{}, kt + 1);
+        tail(P1{}, kt + 1);
+        if (kt + 2 >= KT) break;
+        head(P0{}, kt + 2);
       }
+      wait_vmcnt<0>();  // the (range-checked) loads of steps KT and KT + 1
+      mfma_drain();
     }
   }
 
@@ -879,7 +879,37 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
     else if (p.act == ACT_GELU_TANH) activate<ACT_GELU_TANH>(acc, e_w);
     else if (p.act == ACT_SILU) activate<ACT_SILU>(acc, e_w);
   }
-  static_for<0, MI * NI>([&](auto I) {
+  // One wave per SIMD, intermediate epilogue, wave tile inside the matrix,
+  // no accumulator export: no per-element bounds checks, and the 16-bit
+  // encoding of two values packed with one byte permute.
+  bool stored = false;
+  if constexpr (NW == 4 && !FUSE && EPI != EPI_DIRECT) {
+    if (!p.acc_out && m0 + wm + 16 * MI <= M && n0 + wn + 16 * NI <= N) {
+      static_for<0, MI * NI>([&](auto I) {
+        constexpr int mi = decltype(I)::value / NI, ni = decltype(I)::value % NI;
+        const v4f v = AccTile<decltype(I)::value>::read();
+        lmax = fmaxf(lmax, fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))));
+        const int64_t e = (int64_t)(mb + 16 * mi) * p.ldw + nb + 16 * ni;
+        if constexpr (EPI == EPI_INTER16) {
+          // bits 16.. of u | ((u & 0xFFFF) + 0xFFFF) are sticky16(u): the
+          // added term sets bit 16 exactly when a lower bit is set
+          uint32_t x[4];
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const uint32_t u = __float_as_uint(v[k]);
+            x[k] = u | ((u & 0xFFFFu) + 0xFFFFu);
+          }
+          *(v2i*)((uint16_t*)p.inter + e) =
+              v2i{(int)__builtin_amdgcn_perm(x[1], x[0], 0x07060302u),
+                  (int)__builtin_amdgcn_perm(x[3], x[2], 0x07060302u)};
+        } else {
+          *(v4f*)((float*)p.inter + e) = v;
+        }
+      });
+      stored = true;
+    }
+  }
+  if (!stored) static_for<0, MI * NI>([&](auto I) {
     constexpr int mi = decltype(I)::value / NI, ni = decltype(I)::value % NI;
     const int m = mb + 16 * mi;
     const int n = nb + 16 * ni;

@@ -228,3 +228,36 @@ def test_config4_square(size, fout):
 @pytest.mark.parametrize("idx", list(range(12)))
 def test_config5_llama_layer(idx):
     _run_case(wl.config_5()[idx], n_samples=16384)
+
+
+# The epilogue has a separate path for wave tiles inside the matrix when the
+# accumulator is not exported (the benchmark's configuration): its codes,
+# scale and statistic must equal those of the exporting path, which the
+# tests above check against the oracle.
+@pytest.mark.parametrize("shape", [(512, 768, 640), (300, 520, 384), (256, 256, 128), (1024, 256, 4096)],
+                         ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("ta,tb", LAYOUTS, ids=lambda v: "T" if v else "N")
+@pytest.mark.parametrize("fout", [sc.E4M3, sc.E5M2, sc.F16])
+def test_no_export_path_matches_export_path(shape, ta, tb, fout):
+    M, N, K = shape
+    say(f"case no-export M={M} N={N} K={K} ta={ta} tb={tb} fout={fout}")
+    A = _rand_codes((M, K), sc.E4M3, 51 + M)
+    B = _rand_codes((K, N), sc.E5M2, 52 + N, heavy=True)
+    A_st = A.t().contiguous() if ta else A
+    B_st = B.t().contiguous() if tb else B
+    r1 = gpu_matmul(A_st, sc.E4M3, ta, 1, B_st, sc.E5M2, tb, -2, fout)
+    r0 = gpu_matmul(A_st, sc.E4M3, ta, 1, B_st, sc.E5M2, tb, -2, fout, want_acc=False)
+    assert np.array_equal(r0[0], r1[0]) and r0[1] == r1[1] and r0[2] == r1[2]
+    check_p1(r1[0], r1[1], r1[2], r1[3], K, 1, -2, fout)
+
+
+def test_no_export_path_headline_8192():
+    case = wl.config_4(8192, sc.E4M3)[0]
+    say(f"case no-export {case.name}")
+    A, B = case.make_a(DEV), case.make_b(DEV)
+    r1 = gpu_matmul(A, case.fa, case.ta, case.a_scale_log2, B, case.fb, case.tb,
+                    case.b_scale_log2, case.fout)
+    r0 = gpu_matmul(A, case.fa, case.ta, case.a_scale_log2, B, case.fb, case.tb,
+                    case.b_scale_log2, case.fout, want_acc=False)
+    assert np.array_equal(r0[0], r1[0]) and r0[1] == r1[1] and r0[2] == r1[2]
+    check_p1(r1[0], r1[1], r1[2], r1[3], case.K, case.a_scale_log2, case.b_scale_log2, case.fout)
