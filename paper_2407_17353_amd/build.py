@@ -44,6 +44,7 @@ def _llvm(tool: str) -> str:
 
 _KERNEL = re.compile(r"^[0-9a-f]+ <(\S+)>:$")
 _AGPR_MFMA = re.compile(r"v_mfma\S* a\[")
+_ANY_AGPR = re.compile(r"\ba\d+\b|\ba\[\d+:\d+\]")
 _COMPILER_AGPR = re.compile(r"v_accvgpr_write_b32 a\d+, v\d+|v_accvgpr_mov_b32|scratch_")
 
 
@@ -71,6 +72,12 @@ def check_accumulator_isolation(obj: str, tmp: str) -> int:
     checked = 0
     for name, body in kernels.items():
         if not any(_AGPR_MFMA.search(l) for l in body):
+            # Every other function (the 8-wave kernels, and the out-of-line
+            # casts the 4-wave epilogues call while accumulators still sit in
+            # AGPRs) must leave AGPRs alone.
+            bad = [l.strip() for l in body if _ANY_AGPR.search(l.split("//")[0])]
+            if bad:
+                raise RuntimeError(f"{obj}: function {name} uses AGPRs: {bad[:4]}")
             continue
         checked += 1
         bad = [l.strip() for l in body if _COMPILER_AGPR.search(l)]
