@@ -75,7 +75,12 @@ hipError_t launch_finalize_amax(const uint32_t* hdr, int e_c, float* amax_out, h
 
 // ---------------------------------------------------------------- GEMM epilogue cast
 
-template <int INTER32, int OUTF>
+// NT: the 16-bit intermediate is larger than the last-level cache (MALL), so it is
+// streamed from HBM with nontemporal loads and the codes written with
+// nontemporal stores, which keeps the cache from thrashing; a smaller
+// intermediate, just written by the GEMM, is still in the MALL and is read
+// through it.
+template <int INTER32, int OUTF, bool NT>
 __global__ __launch_bounds__(EW_THREADS) void epilogue_cast_kernel(EpilogueParams p) {
   const uint32_t amax_raw = p.hdr[0];  // max |w| bits
   const int e_ab = (int)p.hdr[1];      // e_w
@@ -97,17 +102,47 @@ __global__ __launch_bounds__(EW_THREADS) void epilogue_cast_kernel(EpilogueParam
     for (int ch = blockIdx.x * EW_THREADS + threadIdx.x; ch < cpr; ch += gridDim.x * EW_THREADS) {
       const int n = ch * 16;
       uint32_t c[16];
+      const int64_t e = (int64_t)m * p.ldw + n;
       if (INTER32) {
-        load16<kF32>(p.inter, (int64_t)m * p.ldw + n, c);
+        if constexpr (NT) {
+          const u4* q = (const u4*)((const uint32_t*)p.inter + e);
+#pragma unroll
+          for (int h = 0; h < 4; ++h) {
+            const u4 v = __builtin_nontemporal_load(q + h);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) c[4 * h + i] = v[i];
+          }
+        } else {
+          load16<kF32>(p.inter, e, c);
+        }
       } else {
-        load16<kF16>(p.inter, (int64_t)m * p.ldw + n, c);  // 16-bit containers
+        if constexpr (NT) {
+          const u4* q = (const u4*)((const uint16_t*)p.inter + e);
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const u4 v = __builtin_nontemporal_load(q + h);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) c[8 * h + i] = (v[i >> 1] >> (16 * (i & 1))) & 0xFFFFu;
+          }
+        } else {
+          load16<kF16>(p.inter, e, c);  // 16-bit containers
+        }
 #pragma unroll
         for (int i = 0; i < 16; ++i) c[i] <<= 16;
       }
       uint32_t w[8];
       encode16<OUTF>(c, shift, scale, fast, sat, w);
       if (n + 16 <= p.N) {
-        store_words16<OUTF>(p.out, (int64_t)m * p.ldc + n, w);
+        if constexpr (NT && OUTF == kF16) {
+          u4* q = (u4*)((uint16_t*)p.out + (int64_t)m * p.ldc + n);
+          __builtin_nontemporal_store(u4{w[0], w[1], w[2], w[3]}, q);
+          __builtin_nontemporal_store(u4{w[4], w[5], w[6], w[7]}, q + 1);
+        } else if constexpr (NT) {
+          __builtin_nontemporal_store(u4{w[0], w[1], w[2], w[3]},
+                                      (u4*)((uint8_t*)p.out + (int64_t)m * p.ldc + n));
+        } else {
+          store_words16<OUTF>(p.out, (int64_t)m * p.ldc + n, w);
+        }
       } else {
         for (int i = 0; i < 16; ++i)
           if (n + i < p.N) store1<OUTF>(p.out, (int64_t)m * p.ldc + n + i, word_code<OUTF>(w, i));
@@ -123,23 +158,41 @@ static int grid_for(int64_t work) {
   return (int)b;
 }
 
+// 16-bit intermediates above this size no longer sit in the 256 MiB MALL
+// after the GEMM has written them. Measured (cast kernel alone): nontemporal
+// access takes a 384 MiB intermediate from 123.5 to 95 us and a 512 MiB one
+// from 182 to 145 us, but a 128 MiB one from 32 to 34 us; for the fp32
+// intermediate of FP16 outputs it made 8192 x 8192 slower (90 -> 110 us), so
+// that one is always read through the caches.
+constexpr int64_t kStreamingBytes = (int64_t)192 << 20;
+
+template <bool NT>
+void launch_cast(const EpilogueParams& p, int inter32, int out_dtype, dim3 g, dim3 b,
+                 hipStream_t s) {
+  if (inter32 && out_dtype == kF16) {
+    hipLaunchKernelGGL((epilogue_cast_kernel<1, kF16, NT>), g, b, 0, s, p);
+  } else if (inter32 && out_dtype == kE4M3) {
+    hipLaunchKernelGGL((epilogue_cast_kernel<1, kE4M3, NT>), g, b, 0, s, p);
+  } else if (inter32) {
+    hipLaunchKernelGGL((epilogue_cast_kernel<1, kE5M2, NT>), g, b, 0, s, p);
+  } else if (out_dtype == kE4M3) {
+    hipLaunchKernelGGL((epilogue_cast_kernel<0, kE4M3, NT>), g, b, 0, s, p);
+  } else {
+    hipLaunchKernelGGL((epilogue_cast_kernel<0, kE5M2, NT>), g, b, 0, s, p);
+  }
+}
+
 hipError_t launch_epilogue_cast(const EpilogueParams& p, int inter32, int out_dtype,
                                 hipStream_t s) {
   const int cpr = (p.N + 15) / 16;
   const int gx = (cpr + EW_THREADS - 1) / EW_THREADS;
   const int gy = p.M < 1 ? 1 : (p.M > 65535 ? 65535 : p.M);
   const dim3 g(gx < 1 ? 1 : gx, gy), b(EW_THREADS);
-  if (inter32 && out_dtype == kF16) {
-    hipLaunchKernelGGL((epilogue_cast_kernel<1, kF16>), g, b, 0, s, p);
-  } else if (inter32 && out_dtype == kE4M3) {
-    hipLaunchKernelGGL((epilogue_cast_kernel<1, kE4M3>), g, b, 0, s, p);
-  } else if (inter32) {
-    hipLaunchKernelGGL((epilogue_cast_kernel<1, kE5M2>), g, b, 0, s, p);
-  } else if (out_dtype == kE4M3) {
-    hipLaunchKernelGGL((epilogue_cast_kernel<0, kE4M3>), g, b, 0, s, p);
-  } else {
-    hipLaunchKernelGGL((epilogue_cast_kernel<0, kE5M2>), g, b, 0, s, p);
-  }
+  const int64_t inter_bytes = (int64_t)p.M * p.ldw * 2;
+  if (!inter32 && inter_bytes > kStreamingBytes)
+    launch_cast<true>(p, inter32, out_dtype, g, b, s);
+  else
+    launch_cast<false>(p, inter32, out_dtype, g, b, s);
   return hipGetLastError();
 }
 
