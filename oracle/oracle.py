@@ -91,6 +91,10 @@ def _load():
     lib.or_fused_pre.argtypes = [vp, c_i64, c_i64, c_f32, c_f32, c_i64, vp, c_int, c_i64, c_f32,
                                  c_int, vp, vp, ctypes.POINTER(c_i32), ctypes.POINTER(c_i32)]
     lib.or_fused_pre.restype = c_int
+    lib.or_fused_pre_ch.argtypes = [vp, c_i64, c_i64, c_f32, c_f32, vp, vp, c_i64, vp, c_int, c_i64,
+                                    c_f32, c_int, vp, vp, ctypes.POINTER(c_i32),
+                                    ctypes.POINTER(c_i32)]
+    lib.or_fused_pre_ch.restype = c_int
     lib.or_finish_pre.argtypes = [vp, c_i64, c_i32, c_i32, c_int, c_i32, c_f32, c_int, c_int, vp,
                                   ctypes.POINTER(c_f32)]
     lib.or_finish_pre.restype = c_i32
@@ -250,12 +254,15 @@ def add_scale_log2(e1: int, e2: int) -> int:
 
 
 def fused_pre(acc: np.ndarray, s_a: float, s_b: float, K: int, residual=None,
-              act: int = ACT_NONE):
+              act: int = ACT_NONE, ch_a=None, ch_b=None):
     """Pre-cast value of the matmul epilogue with a fused scaled add and
     activation (Algorithm 3 add rule, Appendix C.1 activation rule).
 
     residual: None or (codes, fmt, scale): codes [M,N] or [1,N] (one row
     repeated, a bias) of format fmt with scalar scale `scale`.
+    ch_a / ch_b: None or channel scales (powers of two), one per row of A
+    ([M]) / per column of B ([N]) (Section 2: a scale broadcastable to the
+    data), folded into w by one power-of-two product of acc.
     Returns (w, y64, e_w, e_cc): w fp32 [M,N] with true value w * 2^e_w,
     y64 the fp64 value before w's last rounding, and e_cc such that the
     rescale statistic is taken over w * 2^-e_cc."""
@@ -266,17 +273,22 @@ def fused_pre(acc: np.ndarray, s_a: float, s_b: float, K: int, residual=None,
     y64 = np.empty((M, N), dtype=np.float64)
     e_w = ctypes.c_int32(0)
     e_cc = ctypes.c_int32(0)
+    ca = None if ch_a is None else np.ascontiguousarray(ch_a, dtype=np.float32).reshape(-1)
+    cb = None if ch_b is None else np.ascontiguousarray(ch_b, dtype=np.float32).reshape(-1)
+    assert ca is None or ca.size == M
+    assert cb is None or cb.size == N
     if residual is None:
-        rc = lib.or_fused_pre(_ptr(acc), M, N, s_a, s_b, int(K), None, 0, 0, 1.0, int(act),
-                              _ptr(w), _ptr(y64), ctypes.byref(e_w), ctypes.byref(e_cc))
+        codes_p, fmt, ld, scale = None, 0, 0, 1.0
     else:
         codes, fmt, scale = residual
         codes = np.ascontiguousarray(codes, dtype=_code_dtype(fmt))
         assert codes.shape in ((M, N), (1, N)), codes.shape
         ld = 0 if codes.shape[0] == 1 and M != 1 else N
-        rc = lib.or_fused_pre(_ptr(acc), M, N, s_a, s_b, int(K), _ptr(codes), int(fmt), ld,
-                              float(scale), int(act), _ptr(w), _ptr(y64), ctypes.byref(e_w),
-                              ctypes.byref(e_cc))
+        codes_p = _ptr(codes)
+    rc = lib.or_fused_pre_ch(_ptr(acc), M, N, s_a, s_b, _ptr(ca) if ca is not None else None,
+                             _ptr(cb) if cb is not None else None, int(K), codes_p, int(fmt), ld,
+                             float(scale), int(act), _ptr(w), _ptr(y64), ctypes.byref(e_w),
+                             ctypes.byref(e_cc))
     if rc != 0:
         raise ValueError("scales must be finite powers of two")
     return w, y64, int(e_w.value), int(e_cc.value)
@@ -298,10 +310,11 @@ def finish_pre(w: np.ndarray, e_w: int, e_cc: int, mode: int = RESCALE_AMAX, tar
 
 
 def matmul_epilogue_fused(acc, s_a, s_b, K, residual=None, act=ACT_NONE, mode=RESCALE_AMAX,
-                          target_log2=0, amax_in=0.0, saturate=True, out_fmt=E4M3):
-    """Matmul epilogue with the fused scaled add and activation, then the
-    rescale and cast. Returns (codes, e_out, amax, w, y64)."""
-    w, y64, e_w, e_cc = fused_pre(acc, s_a, s_b, K, residual, act)
+                          target_log2=0, amax_in=0.0, saturate=True, out_fmt=E4M3,
+                          ch_a=None, ch_b=None):
+    """Matmul epilogue with the channel scales, the fused scaled add and the
+    activation, then the rescale and cast. Returns (codes, e_out, amax, w, y64)."""
+    w, y64, e_w, e_cc = fused_pre(acc, s_a, s_b, K, residual, act, ch_a, ch_b)
     codes, e_out, amax = finish_pre(w, e_w, e_cc, mode, target_log2, amax_in, saturate, out_fmt)
     return codes, e_out, amax, w, y64
 

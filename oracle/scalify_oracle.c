@@ -564,11 +564,34 @@ int32_t or_add_scale_log2(int32_t e1, int32_t e2)
  * y64[i] (optional) receives the unrounded fp64 value before that last
  * rounding (w itself without an activation).
  * Returns 0, or -1 on a scale that is not a finite power of two. */
+int or_fused_pre_ch(const float* acc, int64_t M, int64_t N, float s_a, float s_b,
+                    const float* ch_a, const float* ch_b, int64_t K,
+                    const void* res, int res_fmt, int64_t res_ld, float s_res, int act,
+                    float* w, double* y64, int32_t* e_w_out, int32_t* e_cc_out);
+
 int or_fused_pre(const float* acc, int64_t M, int64_t N, float s_a, float s_b, int64_t K,
                  const void* res, int res_fmt, int64_t res_ld, float s_res, int act,
                  float* w, double* y64, int32_t* e_w_out, int32_t* e_cc_out)
 {
-    int ok_a = 1, ok_b = 1, ok_r = 1;
+    return or_fused_pre_ch(acc, M, N, s_a, s_b, NULL, NULL, K, res, res_fmt, res_ld, s_res, act,
+                           w, y64, e_w_out, e_cc_out);
+}
+
+/* or_fused_pre with channel scales (Section 2: a scale broadcastable to the
+ * data; channel scaling): A = A_d * s_a * ch_a[i] (ch_a: one power of two per
+ * row of A, i.e. per output row; NULL = all 1), B = B_d * s_b * ch_b[j] (one
+ * per column of B, i.e. per output column). The output keeps one scalar
+ * scale: the channel factors go into the data, as one power-of-two product
+ * of acc (exact unless it leaves the fp32 range):
+ *   no residual: w = fl32(acc * ch_a[i] * ch_b[j]);
+ *   residual: the product term is fl32(acc * 2^(e_a+e_b-e_w) * ch_a[i] * ch_b[j])
+ *     (one power-of-two product) before the scaled add. */
+int or_fused_pre_ch(const float* acc, int64_t M, int64_t N, float s_a, float s_b,
+                    const float* ch_a, const float* ch_b, int64_t K,
+                    const void* res, int res_fmt, int64_t res_ld, float s_res, int act,
+                    float* w, double* y64, int32_t* e_w_out, int32_t* e_cc_out)
+{
+    int ok_a = 1, ok_b = 1, ok_r = 1, ok_ch = 1;
     int32_t e_a = or_scale_exponent(s_a, &ok_a);
     int32_t e_b = or_scale_exponent(s_b, &ok_b);
     int32_t e_c = or_matmul_scale_log2(K);
@@ -576,6 +599,17 @@ int or_fused_pre(const float* acc, int64_t M, int64_t N, float s_a, float s_b, i
     int32_t e_w, e_cc;
     int64_t i, j;
     if (!ok_a || !ok_b || !ok_r) return -1;
+    for (i = 0; ch_a && i < M; ++i) {
+        int ok = 1;
+        (void)or_scale_exponent(ch_a[i], &ok);
+        ok_ch &= ok;
+    }
+    for (j = 0; ch_b && j < N; ++j) {
+        int ok = 1;
+        (void)or_scale_exponent(ch_b[j], &ok);
+        ok_ch &= ok;
+    }
+    if (!ok_ch) return -1;
     if (res) {
         e_w = or_add_scale_log2(e_a + e_b + e_c, q);
         e_cc = 0;
@@ -588,12 +622,16 @@ int or_fused_pre(const float* acc, int64_t M, int64_t N, float s_a, float s_b, i
             int64_t k = i * N + j;
             double y;
             float v = acc[k];
+            int32_t e_ch = (ch_a ? or_scale_exponent(ch_a[i], &ok_ch) : 0) +
+                           (ch_b ? or_scale_exponent(ch_b[j], &ok_ch) : 0);
             if (res) {
                 int64_t rk = i * res_ld + j;
                 uint32_t c = res_fmt == OR_F16 ? ((const uint16_t*)res)[rk]
                                                : ((const uint8_t*)res)[rk];
                 float r = (float)or_decode(res_fmt, c);
-                v = (float)((double)ldexpf(v, e_a + e_b - e_w) + (double)ldexpf(r, q - e_w));
+                v = (float)((double)ldexpf(v, e_a + e_b - e_w + e_ch) + (double)ldexpf(r, q - e_w));
+            } else if (e_ch != 0) {
+                v = ldexpf(v, e_ch);
             }
             y = (double)v;
             if (act != OR_ACT_NONE) y = (double)v * or_gate(act, ldexp((double)v, e_w));
