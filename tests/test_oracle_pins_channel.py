@@ -72,7 +72,7 @@ def test_moving_a_power_of_two_between_scalar_and_channel_scale(with_residual, a
         normal = (np.abs(w0) >= 2.0 ** -126) & (np.abs(w1) >= 2.0 ** -126)
         assert np.array_equal((w1.astype(np.float64) * 2.0 ** e1)[normal],
                               (w0.astype(np.float64) * 2.0 ** e0)[normal])
-        assert normal.sum() >= normal.size - 4
+        assert np.array_equal(w1 == 0, w0 == 0) or act != orc.ACT_NONE
 
 
 def test_unit_channel_scales_reduce_to_the_scalar_path():
