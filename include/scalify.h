@@ -125,6 +125,13 @@ typedef struct {
     float* pre_out;      /* optional validation output: device fp32 [M][N], the value w the
                             rescale and cast see (after the add and the activation), whose
                             true value is w * 2^e_w (e_w as in scalify_matmul) */
+    const float* a_channel_scale; /* optional channel scales of a (Section 2: a scale
+                            broadcastable to the data; channel scaling): device fp32 [M],
+                            one power of two (exponent in [-149, 127]) per row of the logical
+                            a, i.e. per output row, on top of *a.scale; NULL = none */
+    const float* b_channel_scale; /* optional: device fp32 [N], one power of two per column
+                            of the logical b (per output column), on top of *b.scale,
+                            16-byte aligned; NULL = none */
 } scalify_matmul_opts;
 
 /* Exponent e_c of the matmul scale rule (Section 3.2, Algorithm 3): the
@@ -140,8 +147,9 @@ int32_t scalify_matmul_scale_log2(int64_t K);
 size_t scalify_matmul_workspace_size(int64_t M, int64_t N, int32_t out_dtype, int32_t rescale);
 
 /* Workspace bytes of a scalify_matmul call with these options: as above, but
- * a call that fuses a residual add or an activation, or asks for pre_out,
- * keeps an fp32 intermediate (4 bytes per element for every output type).
+ * a call that fuses a residual add or an activation, has channel scales, or
+ * asks for pre_out, keeps an fp32 intermediate (4 bytes per element for
+ * every output type).
  * Returns 0 for invalid arguments or a NULL opts. */
 size_t scalify_matmul_workspace_size_opts(int64_t M, int64_t N, const scalify_matmul_opts* opts);
 
@@ -163,6 +171,14 @@ size_t scalify_matmul_workspace_size_opts(int64_t M, int64_t N, const scalify_ma
  *   out.data  = RNE(acc * 2^(e_a + e_b - e_out)) in out.dtype (saturating
  *               when opts.saturate), *out.scale = 2^e_out
  * so that dec(out) * s_out = s_a * s_b * acc up to the final rounding.
+ *
+ * Channel scales (opts.a_channel_scale = c, opts.b_channel_scale = d): a[i,k]
+ * = dec(a)[i,k] * s_a * c[i], b[k,j] = dec(b)[k,j] * s_b * d[j]. The output
+ * keeps one scalar scale: the channel factors go into the data as one
+ * power-of-two product of acc (exact unless it leaves the fp32 range),
+ * w = fl32(acc * c[i] * d[j]) in place of acc below (with a residual, the
+ * product term is fl32(acc * 2^(e_a+e_b-e_w) * c[i] * d[j])); such a call
+ * keeps an fp32 intermediate like a fused one.
  *
  * Fused scaled add and activation (opts.residual, opts.activation): the
  * epilogue first forms w, whose true value is w * 2^e_w, then rescales and

@@ -48,7 +48,8 @@ class CMatmulOpts(ctypes.Structure):
                 ("acc_out", ctypes.c_void_p), ("amax_out", ctypes.c_void_p),
                 ("events", ctypes.c_void_p), ("amax_in", ctypes.c_void_p),
                 ("residual", ctypes.POINTER(CScaledArray)), ("activation", ctypes.c_int32),
-                ("pre_out", ctypes.c_void_p)]
+                ("pre_out", ctypes.c_void_p), ("a_channel_scale", ctypes.c_void_p),
+                ("b_channel_scale", ctypes.c_void_p)]
 
 
 EXPORTED = ("scalify_matmul_scale_log2", "scalify_matmul_workspace_size",
@@ -178,7 +179,8 @@ def scalify_matmul(a: ScaledArray, b: ScaledArray, out: ScaledArray, *, rescale:
                    target_log2: int = 0, saturate: bool = True, acc_out: torch.Tensor = None,
                    amax_out: torch.Tensor = None, amax_in: torch.Tensor = None,
                    residual: "ScaledArray" = None, activation: int = ACT_NONE,
-                   pre_out: torch.Tensor = None,
+                   pre_out: torch.Tensor = None, a_channel_scale: torch.Tensor = None,
+                   b_channel_scale: torch.Tensor = None,
                    ws: torch.Tensor = None, stream=None, events=None) -> None:
     """Scaled matmul (Section 3.2) with the fused dynamic or delayed rescale
     and cast (Section 3.3); see scalify_matmul in include/scalify.h.
@@ -187,7 +189,9 @@ def scalify_matmul(a: ScaledArray, b: ScaledArray, out: ScaledArray, *, rescale:
     `residual`: ScaledArray [M, N] added by the scaled add rule before the
     `activation` (ACT_*); a row broadcast as `bias.expand(M, N)` (stride 0)
     adds one row to every row. `pre_out`: fp32 [M, N] device tensor that
-    receives the pre-cast value w (validation).
+    receives the pre-cast value w (validation). `a_channel_scale` /
+    `b_channel_scale`: contiguous fp32 device tensors [M] / [N] of powers of
+    two, channel scales of a's rows / b's columns.
     `events`: an optional sequence of 3 torch.cuda.Event(enable_timing=True)
     recorded before the GEMM kernel, after it and after the epilogue (None
     entries are skipped)."""
@@ -205,7 +209,9 @@ def scalify_matmul(a: ScaledArray, b: ScaledArray, out: ScaledArray, *, rescale:
                        amax_out.data_ptr() if amax_out is not None else None,
                        ctypes.cast(ev_arr, ctypes.c_void_p) if ev_arr is not None else None,
                        amax_in.data_ptr() if amax_in is not None else None,
-                       None, int(activation), pre_out.data_ptr() if pre_out is not None else None)
+                       None, int(activation), pre_out.data_ptr() if pre_out is not None else None,
+                       a_channel_scale.data_ptr() if a_channel_scale is not None else None,
+                       b_channel_scale.data_ptr() if b_channel_scale is not None else None)
     cr = residual.c_struct() if residual is not None else None
     if cr is not None:
         opts.residual = ctypes.pointer(cr)

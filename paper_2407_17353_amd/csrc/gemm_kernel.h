@@ -498,9 +498,64 @@ __device__ __forceinline__ float smooth_gate(float x) {
 // w * 2^e_w. One straight pass per transformation. The residual codes of all
 // the wave's outputs are loaded first, so that their latencies overlap; a
 // wave tile inside the matrix loads them without per-output checks.
-template <int RF, int MI_, int NI_>
+// Exponent of a power of two held in fp32 (normal or subnormal encoding).
+__device__ __forceinline__ int pow2_exponent_of(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const int e = (int)((u >> 23) & 0xFFu);
+  if (e != 0) return e - 127;
+  const uint32_t m = u & 0x7FFFFFu;
+  return m ? (31 - __clz((int)m)) - 149 : -127;
+}
+
+// Channel exponents of a wave's outputs, packed 4 to a register as e + 128
+// (channel scales lie in the E8M0 range [2^-127, 2^127]): cha[mi] for the
+// row block (rows mb + 16 mi), chb[ni] byte i for column nb + 16 ni + i; 0
+// where there is no channel scale or the output lies outside the matrix.
+// All loads are issued before the first use; the packed form keeps the
+// registers free for the residual codes loaded next.
+template <int MI_, int NI_>
+__device__ __forceinline__ void load_channel_exponents(const GemmParams& p, int mb, int nb,
+                                                       int (&cha)[MI_], uint32_t (&chb)[NI_]) {
+  float va[MI_];
+  v4f vb[NI_];
+#pragma unroll
+  for (int mi = 0; mi < MI_; ++mi) {
+    const int m = mb + 16 * mi;
+    va[mi] = (p.ch_a && m < p.M) ? p.ch_a[m] : 1.0f;
+  }
+#pragma unroll
+  for (int ni = 0; ni < NI_; ++ni) {
+    const int n = nb + 16 * ni;
+    if (p.ch_b && n + 3 < p.N) {
+      vb[ni] = *(const v4f*)(p.ch_b + n);
+    } else {
+      vb[ni] = v4f{1.f, 1.f, 1.f, 1.f};
+      if (p.ch_b) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (n + i < p.N) vb[ni][i] = p.ch_b[n + i];
+      }
+    }
+  }
+#pragma unroll
+  for (int mi = 0; mi < MI_; ++mi) cha[mi] = pow2_exponent_of(va[mi]);
+#pragma unroll
+  for (int ni = 0; ni < NI_; ++ni) {
+    uint32_t w = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) w |= (uint32_t)(pow2_exponent_of(vb[ni][i]) + 128) << (8 * i);
+    chb[ni] = w;
+  }
+}
+
+__device__ __forceinline__ int chb_exp(uint32_t packed, int i) {
+  return (int)((packed >> (8 * i)) & 0xFFu) - 128;
+}
+
+template <int RF, bool CH, int MI_, int NI_>
 __device__ __forceinline__ void add_residual(const GemmParams& p, v4f (&acc)[MI_][NI_], int mb,
-                                             int nb, bool interior, int sh_acc, int sh_res) {
+                                             int nb, bool interior, int sh_acc, int sh_res,
+                                             const int (&cha)[MI_], const uint32_t (&chb)[NI_]) {
   constexpr int W = RF == kF16 ? 2 : 1;  // code words per 4 outputs
   uint32_t rc[MI_][NI_][W];
   if (interior) {
@@ -530,7 +585,9 @@ __device__ __forceinline__ void add_residual(const GemmParams& p, v4f (&acc)[MI_
     constexpr int mi = decltype(I)::value / NI_, ni = decltype(I)::value % NI_;
     const v4f r = decode_residual4(RF, rc[mi][ni][0], rc[mi][ni][W - 1]);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) acc[mi][ni][i] = ldexpf(acc[mi][ni][i], sh_acc) + ldexpf(r[i], sh_res);
+    for (int i = 0; i < 4; ++i)
+      acc[mi][ni][i] = ldexpf(acc[mi][ni][i], CH ? sh_acc + cha[mi] + chb_exp(chb[ni], i) : sh_acc) +
+                       ldexpf(r[i], sh_res);
     __builtin_amdgcn_sched_barrier(0);  // one group at a time: bounded register use
   });
 }
@@ -552,9 +609,12 @@ __device__ __forceinline__ void activate(v4f (&acc)[MI_][NI_], int e_w) {
   });
 }
 
-template <bool A_MN, bool B_KC, int FA, int FB, int EPI, bool FUSE, int NW>
+// CH: the fused epilogue also applies channel scales (instantiated apart, so
+// that the other fused kernels keep their register allocation).
+template <bool A_MN, bool B_KC, int FA, int FB, int EPI, bool FUSE, int NW, bool CH = false>
 __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
   static_assert(NW == 8 || (NW == 4 && !FUSE), "the fused epilogue runs on the 8-wave kernel");
+  static_assert(FUSE || !CH, "channel scales are part of the fused epilogue");
   using C = WaveCfg<NW>;
   constexpr int WAVES = C::WAVES, WAVES_N = C::WAVES_N, WTM = C::WTM, WTN = C::WTN;
   constexpr int MI = C::MI, NI = C::NI, BPW = C::BPW, LOADS_PER_STEP = C::LOADS_PER_STEP;
@@ -867,13 +927,30 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
         }
       });
     }
+    // Channel scales (CH): one power-of-two product of the accumulator,
+    // folded into the scaled add's shift when there is a residual.
+    int cha[MI] = {};
+    uint32_t chb[NI] = {};
+    if constexpr (CH) {
+      load_channel_exponents(p, mb, nb, cha, chb);
+      __builtin_amdgcn_sched_barrier(0);
+    } else {
+#pragma unroll
+      for (int ni = 0; ni < NI; ++ni) chb[ni] = 0x80808080u;  // exponent 0
+    }
     if (p.res) {
       const bool interior = m0 + wm + 16 * MI <= M && n0 + wn + 16 * NI <= N;
       const int sh_acc = (int)__builtin_amdgcn_readfirstlane(p.hdr[3]);
       const int sh_res = (int)__builtin_amdgcn_readfirstlane(p.hdr[4]);
-      if (p.res_fmt == kE4M3) add_residual<kE4M3>(p, acc, mb, nb, interior, sh_acc, sh_res);
-      else if (p.res_fmt == kE5M2) add_residual<kE5M2>(p, acc, mb, nb, interior, sh_acc, sh_res);
-      else add_residual<kF16>(p, acc, mb, nb, interior, sh_acc, sh_res);
+      if (p.res_fmt == kE4M3) add_residual<kE4M3, CH>(p, acc, mb, nb, interior, sh_acc, sh_res, cha, chb);
+      else if (p.res_fmt == kE5M2) add_residual<kE5M2, CH>(p, acc, mb, nb, interior, sh_acc, sh_res, cha, chb);
+      else add_residual<kF16, CH>(p, acc, mb, nb, interior, sh_acc, sh_res, cha, chb);
+    } else if constexpr (CH) {
+      static_for<0, MI * NI>([&](auto I) {
+        constexpr int mi = decltype(I)::value / NI, ni = decltype(I)::value % NI;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[mi][ni][i] = ldexpf(acc[mi][ni][i], cha[mi] + chb_exp(chb[ni], i));
+      });
     }
     if (p.act == ACT_RELU) activate<ACT_RELU>(acc, e_w);
     else if (p.act == ACT_GELU_TANH) activate<ACT_GELU_TANH>(acc, e_w);
@@ -1020,6 +1097,12 @@ template <bool A_MN, bool B_KC, bool FUSE, int FA, int FB, int EPI>
 hipError_t launch_epi(const GemmParams& p, hipStream_t s) {
   constexpr int NW = gemm_waves(EPI, FUSE);
   const dim3 grid(p.tiles_m * p.tiles_n), block(WaveCfg<NW>::NTHR);
+  if constexpr (FUSE) {
+    if (p.ch_a || p.ch_b) {
+      hipLaunchKernelGGL((gemm_kernel<A_MN, B_KC, FA, FB, EPI, FUSE, NW, true>), grid, block, 0, s, p);
+      return hipGetLastError();
+    }
+  }
   hipLaunchKernelGGL((gemm_kernel<A_MN, B_KC, FA, FB, EPI, FUSE, NW>), grid, block, 0, s, p);
   return hipGetLastError();
 }

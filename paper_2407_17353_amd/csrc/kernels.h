@@ -49,6 +49,11 @@ struct GemmParams {
   int res_fmt;
   int act;
   float* pre_out;
+  // Channel scales (FUSE kernels only): powers of two per output row
+  // (ch_a [M]) and per output column (ch_b [N]) multiplied into the
+  // accumulator with the power-of-two product of the epilogue; NULL = 1.
+  const float* ch_a;
+  const float* ch_b;
 };
 
 // fuse: launch the kernels with the fused residual add / activation / pre_out

@@ -48,7 +48,8 @@ size_t matmul_ws(int64_t M, int64_t N, int32_t out_dtype, int32_t rescale, bool 
 }
 
 bool is_fused(const scalify_matmul_opts* o) {
-  return o->residual != nullptr || o->activation != SCALIFY_ACT_NONE || o->pre_out != nullptr;
+  return o->residual != nullptr || o->activation != SCALIFY_ACT_NONE || o->pre_out != nullptr ||
+         o->a_channel_scale != nullptr || o->b_channel_scale != nullptr;
 }
 
 // Residual of the fused scaled add: M x N, row-major, ld = 0 (one row for
@@ -184,6 +185,8 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
   if ((st = check_matrix(out, out->dtype == SCALIFY_F16 ? 8 : 16)) != SCALIFY_OK) return st;
   const scalify_scaled_array* res = opts->residual;
   if (res && (st = check_residual(res, out, M, N)) != SCALIFY_OK) return st;
+  if (!aligned16(opts->b_channel_scale) || ((uintptr_t)opts->a_channel_scale & 3u))
+    return SCALIFY_ERR_ALIGN;
   const bool fused = is_fused(opts);
   // 32-bit byte offsets inside the GEMM kernel, including the range-checked
   // reads of up to one tile past the last stored row.
@@ -246,6 +249,8 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
   p.res_fmt = res ? res->dtype : 0;
   p.act = opts->activation;
   p.pre_out = opts->pre_out;
+  p.ch_a = opts->a_channel_scale;
+  p.ch_b = opts->b_channel_scale;
   hipEvent_t* ev = (hipEvent_t*)opts->events;
   if (ev && ev[0] && hipEventRecord(ev[0], s) != hipSuccess) return SCALIFY_ERR_HIP;
   if (M > 0 && N > 0) {

@@ -77,6 +77,7 @@ def call_matmul(a, b, out, opts=None, ws=FAKE + 8192, ws_bytes=1 << 40):
     ("bad_mode", 7), ("delayed_without_statistic", 1), ("bad_target", 7), ("out_trans", 4), ("k_mismatch", 3), ("n_mismatch", 3),
     ("negative", 3), ("ld_small", 3), ("ld_unaligned", 5), ("ptr_unaligned", 5),
     ("ws_small", 6), ("ws_null", 6), ("ws_unaligned", 6), ("null_data", 1), ("too_big", 3),
+    ("channel_b_unaligned", 5), ("channel_a_unaligned", 5),
 ])
 def test_matmul_argument_errors(case, status):
     a, b, out = arr(64, 128), arr(128, 32), arr(64, 32)
@@ -119,6 +120,14 @@ def test_matmul_argument_errors(case, status):
         a = arr(64, 128, data=None)
     elif case == "too_big":
         a, b, out = arr(1 << 17, 1 << 15), arr(1 << 15, 32), arr(1 << 17, 32)
+    elif case == "channel_b_unaligned":
+        o = sc.CMatmulOpts(sc.E4M3, 1, 0, 1)
+        o.b_channel_scale = FAKE + 20
+        kw["opts"] = o
+    elif case == "channel_a_unaligned":
+        o = sc.CMatmulOpts(sc.E4M3, 1, 0, 1)
+        o.a_channel_scale = FAKE + 2
+        kw["opts"] = o
     assert call_matmul(a, b, out, **kw) == status
 
 
@@ -168,6 +177,10 @@ def test_fused_workspace_sizes():
     assert sc.scalify_matmul_workspace_size_opts(17, 33, sc.E5M2, fused=True) == 256 + 17 * 48 * 4
     assert sc.scalify_matmul_workspace_size_opts(10, 10, sc.F16, fused=True) == 256 + 10 * 16 * 4
     assert sc.scalify_matmul_workspace_size_opts(10, 10, sc.E4M3, sc.RESCALE_DELAYED, True) == 256
+    # channel scales keep the fp32 intermediate as well
+    o = sc.CMatmulOpts(sc.E4M3, sc.RESCALE_AMAX, 0, 1)
+    o.b_channel_scale = FAKE
+    assert sc.load_library().scalify_matmul_workspace_size_opts(10, 10, ctypes.byref(o)) == 256 + 10 * 16 * 4
     assert sc.load_library().scalify_matmul_workspace_size_opts(10, 10, None) == 0
 
 

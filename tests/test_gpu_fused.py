@@ -61,8 +61,9 @@ def _residual_device(codes, fmt, M):
 
 
 def _run(A, fa, ta, sa, B, fb, tb, sb, fout, *, res=None, act=sc.ACT_NONE, mode=sc.RESCALE_AMAX,
-         target=0, sat=True, amax_in=0.0, inplace=False, want_pre=True):
-    """One fused scalify_matmul call. res = (codes, fmt, scale_log2) or None.
+         target=0, sat=True, amax_in=0.0, inplace=False, want_pre=True, ch_a=None, ch_b=None):
+    """One fused scalify_matmul call. res = (codes, fmt, scale_log2) or None;
+    ch_a / ch_b: numpy channel scales ([M] / [N] powers of two) or None.
     Returns codes, e_out, amax, acc, pre (w), K."""
     a = sc.ScaledArray(stored_with_padding(A, DEV), fa, sc.scale_tensor(sa, DEV), ta)
     b = sc.ScaledArray(stored_with_padding(B, DEV), fb, sc.scale_tensor(sb, DEV), tb)
@@ -83,7 +84,8 @@ def _run(A, fa, ta, sa, B, fb, tb, sb, fout, *, res=None, act=sc.ACT_NONE, mode=
     stat_out = torch.empty(1, dtype=torch.float32, device=DEV)
     sc.scalify_matmul(a, b, out, rescale=mode, target_log2=target, saturate=sat, acc_out=acc,
                       amax_out=stat_out, amax_in=stat_in if mode == sc.RESCALE_DELAYED else None,
-                      residual=residual, activation=act, pre_out=pre)
+                      residual=residual, activation=act, pre_out=pre,
+                      a_channel_scale=_dev_f32(ch_a), b_channel_scale=_dev_f32(ch_b))
     torch.cuda.synchronize()
     codes = out.data.cpu().numpy()
     if fout == sc.F16:
@@ -93,6 +95,10 @@ def _run(A, fa, ta, sa, B, fb, tb, sb, fout, *, res=None, act=sc.ACT_NONE, mode=
     assert s == 2.0 ** e_out
     return (codes.copy(), e_out, float(stat_out.item()), acc.cpu().numpy(),
             pre.cpu().numpy() if want_pre else None, K)
+
+
+def _dev_f32(x):
+    return None if x is None else torch.from_numpy(np.asarray(x, dtype=np.float32)).to(DEV)
 
 
 def _oracle_res(res):
@@ -111,12 +117,13 @@ def _gate_arg(act, x):
         return x
 
 
-def check_fused(run, sa, sb, fout, res, act, mode, target=0, sat=True, amax_in=0.0):
+def check_fused(run, sa, sb, fout, res, act, mode, target=0, sat=True, amax_in=0.0, ch_a=None,
+                ch_b=None):
     """F1 and F2 for one call's outputs; returns the number of elements of w
     that differ from the oracle's value (gelu / silu only)."""
     codes, e_out, amax, acc, pre, K = run
     ores = _oracle_res(res)
-    w_ref, y64, e_w, e_cc = orc.fused_pre(acc, 2.0 ** sa, 2.0 ** sb, K, ores, act)
+    w_ref, y64, e_w, e_cc = orc.fused_pre(acc, 2.0 ** sa, 2.0 ** sb, K, ores, act, ch_a, ch_b)
     # F1
     nan_g, nan_r = np.isnan(pre), np.isnan(y64)
     assert np.array_equal(nan_g, nan_r), "F1: NaN pattern of w differs"
@@ -125,7 +132,7 @@ def check_fused(run, sa, sb, fout, res, act, mode, target=0, sat=True, amax_in=0
             f"F1: w differs at {np.flatnonzero((pre != w_ref) & ~nan_g)[:5]}"
         n_diff = 0
     else:
-        w0, _, _, _ = orc.fused_pre(acc, 2.0 ** sa, 2.0 ** sb, K, ores, sc.ACT_NONE)
+        w0, _, _, _ = orc.fused_pre(acc, 2.0 ** sa, 2.0 ** sb, K, ores, sc.ACT_NONE, ch_a, ch_b)
         fin = ~nan_r
         x = w0.astype(np.float64)[fin] * 2.0 ** e_w
         t = np.abs(_gate_arg(act, x))
