@@ -72,6 +72,12 @@ def _load():
                                   c_i64, c_i64, c_i64, vp]
     lib.or_matmul_acc_at.argtypes = [vp, c_int, c_int, c_i64, vp, c_int, c_int, c_i64,
                                      c_i64, vp, vp, c_i64, vp, vp, vp]
+    lib.or_matmul_acc_mx.argtypes = [vp, c_int, c_int, c_i64, vp, c_int, c_int, c_i64,
+                                     c_i64, c_i64, c_i64, vp, vp, c_i64, vp]
+    lib.or_matmul_acc_mx.restype = c_int
+    lib.or_matmul_acc_mx_at.argtypes = [vp, c_int, c_int, c_i64, vp, c_int, c_int, c_i64,
+                                        c_i64, vp, vp, c_i64, vp, vp, c_i64, vp, vp]
+    lib.or_matmul_acc_mx_at.restype = c_int
     lib.or_matmul_epilogue.argtypes = [vp, c_i64, c_f32, c_f32, c_i64, c_int, c_i32, c_int,
                                        c_int, vp, ctypes.POINTER(c_i32), ctypes.POINTER(c_f32)]
     lib.or_matmul_epilogue.restype = c_int
@@ -189,6 +195,61 @@ def matmul_acc_at(A, fa, ta, B, fb, tb, ii, jj, l1=False):
     lib.or_matmul_acc_at(_ptr(A), fa, int(ta), lda, _ptr(B), fb, int(tb), ldb, K,
                          _ptr(ii), _ptr(jj), ii.size, _ptr(acc), _ptr(t2), _ptr(t1))
     return acc, (t1 if l1 else t2)
+
+
+def mx_block_scale_ld(K: int) -> int:
+    """Row length (bytes) of an MX block-scale array for depth K: one byte
+    per 32 k, padded to whole 128-k steps (4 bytes each)."""
+    return 4 * ((K + 127) // 128)
+
+
+def _mx_scales(sa, sb, M, N, K):
+    sa = np.ascontiguousarray(sa, dtype=np.uint8)
+    sb = np.ascontiguousarray(sb, dtype=np.uint8)
+    ld = sa.shape[1]
+    assert sa.shape[0] == M and sb.shape == (N, ld) and ld >= (K + 31) // 32, (sa.shape, sb.shape)
+    return sa, sb, ld
+
+
+def matmul_acc_mx(A, fa, ta, B, fb, tb, sa, sb) -> np.ndarray:
+    """fp32 accumulator of the FP8 dot_general with MX block scales
+    (Section 2: block scaling formats as scales broadcastable to the data):
+    sa[i, k // 32] and sb[j, k // 32] are E8M0 bytes (value 2^(byte - 127))
+    multiplying A[i, k] and B[k, j]; fp64 sum over ascending k, one rounding
+    to fp32. sa is [M][ld], sb [N][ld], ld >= ceil(K / 32). Raises on an
+    0xFF (NaN) byte among those used."""
+    lib = _load()
+    A, lda = _operand(A, ta)
+    B, ldb = _operand(B, tb)
+    M, K = (A.shape[1], A.shape[0]) if ta else A.shape
+    K2, N = (B.shape[1], B.shape[0]) if tb else B.shape
+    assert K == K2, (K, K2)
+    sa, sb, ld = _mx_scales(sa, sb, M, N, K)
+    acc = np.empty((M, N), dtype=np.float32)
+    if lib.or_matmul_acc_mx(_ptr(A), fa, int(ta), lda, _ptr(B), fb, int(tb), ldb, M, N, K,
+                            _ptr(sa), _ptr(sb), ld, _ptr(acc)):
+        raise ValueError("0xFF is not an E8M0 scale")
+    return acc
+
+
+def matmul_acc_mx_at(A, fa, ta, B, fb, tb, sa, sb, ii, jj):
+    """matmul_acc_mx at sampled positions (ii[p], jj[p]), with the sum of
+    the magnitudes of the scaled product terms at each."""
+    lib = _load()
+    A, lda = _operand(A, ta)
+    B, ldb = _operand(B, tb)
+    M, K = (A.shape[1], A.shape[0]) if ta else A.shape
+    N = B.shape[0] if tb else B.shape[1]
+    sa, sb, ld = _mx_scales(sa, sb, M, N, K)
+    ii = np.ascontiguousarray(ii, dtype=np.int64)
+    jj = np.ascontiguousarray(jj, dtype=np.int64)
+    acc = np.empty(ii.shape, dtype=np.float32)
+    t1 = np.empty(ii.shape, dtype=np.float64)
+    if lib.or_matmul_acc_mx_at(_ptr(A), fa, int(ta), lda, _ptr(B), fb, int(tb), ldb, K,
+                               _ptr(sa), _ptr(sb), ld, _ptr(ii), _ptr(jj), ii.size,
+                               _ptr(acc), _ptr(t1)):
+        raise ValueError("0xFF is not an E8M0 scale")
+    return acc, t1
 
 
 def matmul_epilogue(acc: np.ndarray, s_a: float, s_b: float, K: int, mode: int = RESCALE_AMAX,

@@ -22,6 +22,8 @@
  *     (Section 3.3, Algorithm 4), statistic = amax.
  *   - set_scaling / get_data_and_scale (Section 3.1).
  *   - FP8 E4M3 / E5M2 and FP16 formats (Section 1, Appendix A), OCP variants.
+ *   - Scales broadcast beyond a scalar (Section 2): per-channel powers of two
+ *     and E8M0 block scales of the MX formats.
  *
  * Readings of the paper where it is silent are listed in the design notes
  * of the repository; the ones used here are restated next to the code.
@@ -317,6 +319,84 @@ void or_matmul_acc_at(const uint8_t* A, int fa, int ta, int64_t lda,
         if (term_l2) term_l2[p] = sqrt(q);
         if (term_l1) term_l1[p] = a1;
     }
+}
+
+/* MX block scales (Section 2: a scale broadcastable to the data covers
+ * block formats such as OCP MX, whose scales are E8M0). Row i of A and
+ * column j of B carry one E8M0 byte per 32 consecutive k: the element
+ * A[i,k] stands for dec(A[i,k]) * 2^(sa[i*ld + k/32] - 127), B[k,j] for
+ * dec(B[k,j]) * 2^(sb[j*ld + k/32] - 127), on top of the scalar scales.
+ * 0xFF (the NaN encoding of E8M0) is not a scale: returns 1 if any byte
+ * that a product uses holds it, else 0. Entries k/32 >= ceil(K/32) of a row
+ * are never read. The sum is that of or_matmul_acc with each exact product
+ * multiplied by its two block factors (exact in fp64: both are powers of
+ * two and the product of two FP8 values has at most 8 significant bits). */
+static int mx_block_ok(const uint8_t* s, int64_t rows, int64_t ld, int64_t nb)
+{
+    int64_t r, b;
+    for (r = 0; r < rows; ++r)
+        for (b = 0; b < nb; ++b)
+            if (s[r * ld + b] == 0xFF) return 0;
+    return 1;
+}
+
+int or_matmul_acc_mx(const uint8_t* A, int fa, int ta, int64_t lda,
+                     const uint8_t* B, int fb, int tb, int64_t ldb,
+                     int64_t M, int64_t N, int64_t K,
+                     const uint8_t* sa, const uint8_t* sb, int64_t lds, float* acc)
+{
+    double da[256], db[256];
+    int64_t i, nb = (K + 31) / 32;
+    if (!mx_block_ok(sa, M, lds, nb) || !mx_block_ok(sb, N, lds, nb)) return 1;
+    or_decode_table8(fa, da);
+    or_decode_table8(fb, db);
+    #pragma omp parallel for schedule(dynamic, 1)
+    for (i = 0; i < M; ++i) {
+        int64_t j, k;
+        for (j = 0; j < N; ++j) {
+            double s = 0.0;
+            for (k = 0; k < K; ++k) {
+                const int e = (int)sa[i * lds + k / 32] - 127 + (int)sb[j * lds + k / 32] - 127;
+                s += ldexp(da[A_AT(i, k)] * db[B_AT(k, j)], e);
+            }
+            acc[i * N + j] = (float)s;
+        }
+    }
+    return 0;
+}
+
+/* The same at listed positions (i, j), with the l1 norm of the scaled
+ * product terms (non-finite terms left out), as or_matmul_acc_at. */
+int or_matmul_acc_mx_at(const uint8_t* A, int fa, int ta, int64_t lda,
+                        const uint8_t* B, int fb, int tb, int64_t ldb, int64_t K,
+                        const uint8_t* sa, const uint8_t* sb, int64_t lds,
+                        const int64_t* ii, const int64_t* jj, int64_t n,
+                        float* acc, double* term_l1)
+{
+    double da[256], db[256];
+    int64_t p, nb = (K + 31) / 32, bad = 0;
+    or_decode_table8(fa, da);
+    or_decode_table8(fb, db);
+    for (p = 0; p < n; ++p) {
+        int64_t b;
+        for (b = 0; b < nb; ++b)
+            if (sa[ii[p] * lds + b] == 0xFF || sb[jj[p] * lds + b] == 0xFF) bad = 1;
+    }
+    if (bad) return 1;
+    #pragma omp parallel for schedule(static)
+    for (p = 0; p < n; ++p) {
+        int64_t i = ii[p], j = jj[p], k;
+        double s = 0.0, a1 = 0.0;
+        for (k = 0; k < K; ++k) {
+            const int e = (int)sa[i * lds + k / 32] - 127 + (int)sb[j * lds + k / 32] - 127;
+            const double t = ldexp(da[A_AT(i, k)] * db[B_AT(k, j)], e);
+            s += t;
+            if (isfinite(t)) a1 += fabs(t);
+        }
+        acc[p] = (float)s;
+        term_l1[p] = a1;
+    }
+    return 0;
 }
 
 /* ------------------------------------------------------------------------ */
