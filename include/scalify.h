@@ -132,7 +132,21 @@ typedef struct {
     const float* b_channel_scale; /* optional: device fp32 [N], one power of two per column
                             of the logical b (per output column), on top of *b.scale,
                             16-byte aligned; NULL = none */
+    const uint8_t* a_block_scale; /* optional MX block scales of a (Section 2: block
+                            scaling formats such as MX as scales broadcastable to the
+                            data): device E8M0 bytes [M][scalify_mx_block_scale_ld(K)],
+                            byte a_block_scale[i * ld + k / 32] (value 2^(byte - 127))
+                            scaling a[i,k] on top of *a.scale; 4-byte aligned; given
+                            together with b_block_scale; NULL = none */
+    const uint8_t* b_block_scale; /* device E8M0 bytes [N][scalify_mx_block_scale_ld(K)],
+                            byte b_block_scale[j * ld + k / 32] scaling b[k,j] (per column
+                            of the logical b); 4-byte aligned; NULL = none */
 } scalify_matmul_opts;
+
+/* Row length in bytes of an MX block-scale array for depth K: one byte per
+ * 32 k, padded to whole 128-k steps, 4 * ceil(K / 128). Bytes of a row at
+ * k / 32 >= ceil(K / 32) are padding, never used. Returns 0 for K < 1. */
+int64_t scalify_mx_block_scale_ld(int64_t K);
 
 /* Exponent e_c of the matmul scale rule (Section 3.2, Algorithm 3): the
  * largest e with 2^e <= sqrt(K) (sqrt(K) rounded down to a power of two),
@@ -147,9 +161,9 @@ int32_t scalify_matmul_scale_log2(int64_t K);
 size_t scalify_matmul_workspace_size(int64_t M, int64_t N, int32_t out_dtype, int32_t rescale);
 
 /* Workspace bytes of a scalify_matmul call with these options: as above, but
- * a call that fuses a residual add or an activation, has channel scales, or
- * asks for pre_out, keeps an fp32 intermediate (4 bytes per element for
- * every output type).
+ * a call that fuses a residual add or an activation, has channel or MX block
+ * scales, or asks for pre_out, keeps an fp32 intermediate (4 bytes per
+ * element for every output type).
  * Returns 0 for invalid arguments or a NULL opts. */
 size_t scalify_matmul_workspace_size_opts(int64_t M, int64_t N, const scalify_matmul_opts* opts);
 
@@ -179,6 +193,20 @@ size_t scalify_matmul_workspace_size_opts(int64_t M, int64_t N, const scalify_ma
  * w = fl32(acc * c[i] * d[j]) in place of acc below (with a residual, the
  * product term is fl32(acc * 2^(e_a+e_b-e_w) * c[i] * d[j])); such a call
  * keeps an fp32 intermediate like a fused one.
+ *
+ * MX block scales (opts.a_block_scale = P, opts.b_block_scale = Q, both or
+ * neither): a[i,k] = dec(a)[i,k] * s_a * 2^(P[i][k/32] - 127), b[k,j] =
+ * dec(b)[k,j] * s_b * 2^(Q[j][k/32] - 127): the matrix cores apply the block
+ * factors to the products, acc = sum_k dec(a)[i,k] dec(b)[k,j]
+ * 2^(P[i][k/32] + Q[j][k/32] - 254), and everything below acts on that acc
+ * (the output keeps one scalar scale). The byte 0xFF (E8M0's NaN) is not a
+ * scale: results of a call that uses one are unspecified. Block factors
+ * that push products or partial sums out of fp32's normal range give what
+ * the matrix cores give there (Inf, or subnormals and zeros). Such a call
+ * keeps an fp32 intermediate; it cannot be combined with a residual, an
+ * activation, pre_out or channel scales (SCALIFY_ERR_VALUE); one of the two
+ * arrays alone is SCALIFY_ERR_NULL (an array of no bytes, M * K or N * K
+ * zero, may be NULL), a pointer not 4-byte aligned SCALIFY_ERR_ALIGN.
  *
  * Fused scaled add and activation (opts.residual, opts.activation): the
  * epilogue first forms w, whose true value is w * 2^e_w, then rescales and

@@ -49,14 +49,16 @@ class CMatmulOpts(ctypes.Structure):
                 ("events", ctypes.c_void_p), ("amax_in", ctypes.c_void_p),
                 ("residual", ctypes.POINTER(CScaledArray)), ("activation", ctypes.c_int32),
                 ("pre_out", ctypes.c_void_p), ("a_channel_scale", ctypes.c_void_p),
-                ("b_channel_scale", ctypes.c_void_p)]
+                ("b_channel_scale", ctypes.c_void_p), ("a_block_scale", ctypes.c_void_p),
+                ("b_block_scale", ctypes.c_void_p)]
 
 
 EXPORTED = ("scalify_matmul_scale_log2", "scalify_matmul_workspace_size",
             "scalify_matmul_workspace_size_opts", "scalify_matmul",
             "scalify_rescale_workspace_size", "scalify_rescale", "scalify_cast",
             "scalify_set_scaling", "scalify_status_string", "scalify_layernorm_fwd",
-            "scalify_layernorm_bwd_workspace_size", "scalify_layernorm_bwd")
+            "scalify_layernorm_bwd_workspace_size", "scalify_layernorm_bwd",
+            "scalify_mx_block_scale_ld")
 
 _lib = None
 
@@ -74,6 +76,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
     lib.scalify_matmul_scale_log2.argtypes = [i64]
     lib.scalify_matmul_scale_log2.restype = i32
+    lib.scalify_mx_block_scale_ld.argtypes = [i64]
+    lib.scalify_mx_block_scale_ld.restype = i64
     lib.scalify_matmul_workspace_size.argtypes = [i64, i64, i32, i32]
     lib.scalify_matmul_workspace_size.restype = ctypes.c_size_t
     lib.scalify_matmul_workspace_size_opts.argtypes = [i64, i64, P(CMatmulOpts)]
@@ -153,6 +157,11 @@ def scalify_matmul_scale_log2(K: int) -> int:
     return int(load_library().scalify_matmul_scale_log2(int(K)))
 
 
+def scalify_mx_block_scale_ld(K: int) -> int:
+    """Row length (bytes) of an MX block-scale array for depth K."""
+    return int(load_library().scalify_mx_block_scale_ld(int(K)))
+
+
 def scalify_matmul_workspace_size(M: int, N: int, out_fmt: int, rescale: int = RESCALE_AMAX) -> int:
     return int(load_library().scalify_matmul_workspace_size(M, N, out_fmt, rescale))
 
@@ -180,7 +189,8 @@ def scalify_matmul(a: ScaledArray, b: ScaledArray, out: ScaledArray, *, rescale:
                    amax_out: torch.Tensor = None, amax_in: torch.Tensor = None,
                    residual: "ScaledArray" = None, activation: int = ACT_NONE,
                    pre_out: torch.Tensor = None, a_channel_scale: torch.Tensor = None,
-                   b_channel_scale: torch.Tensor = None,
+                   b_channel_scale: torch.Tensor = None, a_block_scale: torch.Tensor = None,
+                   b_block_scale: torch.Tensor = None,
                    ws: torch.Tensor = None, stream=None, events=None) -> None:
     """Scaled matmul (Section 3.2) with the fused dynamic or delayed rescale
     and cast (Section 3.3); see scalify_matmul in include/scalify.h.
@@ -191,7 +201,10 @@ def scalify_matmul(a: ScaledArray, b: ScaledArray, out: ScaledArray, *, rescale:
     adds one row to every row. `pre_out`: fp32 [M, N] device tensor that
     receives the pre-cast value w (validation). `a_channel_scale` /
     `b_channel_scale`: contiguous fp32 device tensors [M] / [N] of powers of
-    two, channel scales of a's rows / b's columns.
+    two, channel scales of a's rows / b's columns. `a_block_scale` /
+    `b_block_scale`: uint8 device tensors [M, ld] / [N, ld] of E8M0 bytes,
+    ld = scalify_mx_block_scale_ld(K), MX block scales (one per 32 k) of
+    a's rows / b's columns.
     `events`: an optional sequence of 3 torch.cuda.Event(enable_timing=True)
     recorded before the GEMM kernel, after it and after the epilogue (None
     entries are skipped)."""
@@ -211,7 +224,13 @@ def scalify_matmul(a: ScaledArray, b: ScaledArray, out: ScaledArray, *, rescale:
                        amax_in.data_ptr() if amax_in is not None else None,
                        None, int(activation), pre_out.data_ptr() if pre_out is not None else None,
                        a_channel_scale.data_ptr() if a_channel_scale is not None else None,
-                       b_channel_scale.data_ptr() if b_channel_scale is not None else None)
+                       b_channel_scale.data_ptr() if b_channel_scale is not None else None,
+                       a_block_scale.data_ptr() if a_block_scale is not None else None,
+                       b_block_scale.data_ptr() if b_block_scale is not None else None)
+    for t, rows in ((a_block_scale, M), (b_block_scale, N)):
+        if t is not None and (t.dtype != torch.uint8 or not t.is_contiguous() or
+                              tuple(t.shape) != (rows, scalify_mx_block_scale_ld(a.shape[1]))):
+            raise ValueError("block scales: contiguous uint8 [rows, scalify_mx_block_scale_ld(K)]")
     cr = residual.c_struct() if residual is not None else None
     if cr is not None:
         opts.residual = ctypes.pointer(cr)

@@ -6,6 +6,12 @@ namespace scalify {
 hipError_t launch_gemm(const GemmParams& p, bool a_mn, bool b_kc, int fa, int fb, int epi,
                        bool fuse, hipStream_t s) {
   if (p.tiles_m * p.tiles_n == 0) return hipSuccess;
+  if (p.mx_a) {
+    if (!a_mn && b_kc) return launch_layout_mx<false, true>(p, fa, fb, epi, s);
+    if (!a_mn && !b_kc) return launch_layout_mx<false, false>(p, fa, fb, epi, s);
+    if (a_mn && b_kc) return launch_layout_mx<true, true>(p, fa, fb, epi, s);
+    return launch_layout_mx<true, false>(p, fa, fb, epi, s);
+  }
   if (fuse) {
     if (!a_mn && b_kc) return launch_layout<false, true, true>(p, fa, fb, epi, s);
     if (!a_mn && !b_kc) return launch_layout<false, false, true>(p, fa, fb, epi, s);

@@ -120,6 +120,21 @@ __device__ __forceinline__ void load_lds16(v4i rsrc, uint32_t voff, uint8_t* lds
 #pragma clang diagnostic pop
 }
 
+// One buffer_load_dword ... lds: lane i's 4 bytes land at M0 + 4 i (the
+// MX block-scale staging; same M0 and ordering rules as load_lds16).
+__device__ __forceinline__ void load_lds4(v4i rsrc, uint32_t voff, uint8_t* lds_base) {
+  const uint32_t lds_addr = (uint32_t)(uintptr_t)(LDS_AS void*)lds_base;
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "buffer_load_dword %1, %2, 0 offen lds"
+      :
+      : "s"(lds_addr), "v"(voff), "s"(rsrc)
+      : "memory", "m0");
+#pragma clang diagnostic pop
+}
+
 // Wait until at most N of this wave's vector memory loads are outstanding
 // (they complete in issue order).
 template <int N>
@@ -198,25 +213,30 @@ __device__ __forceinline__ void zero_tail_kc(uint8_t* lds, int krem, int tid) {
   for (int b = krem & 15; b < 16; ++b) chunk[b] = 0;
 }
 
-// 32 consecutive k of one row (KC) or one column (MC) of a 16-wide
-// fragment, in the order the MFMA expects: lane l serves row/col (l & 15),
-// k = 32 * (l >> 4) + 0..31.
-template <bool KC>
+// 32 k of one row (KC) or one column (MC) of a 16-wide fragment: lane l
+// serves row/col (l & 15). The sum over k does not depend on which lane
+// holds which k as long as A and B agree, so the plain kernels give lane
+// group g = l >> 4 the k = 32 g + 0..31. The MFMA itself orders its 128 k
+// as byte j of register half h of lane group g <-> k = 64 h + 16 g + j, and
+// its block scale b (from lane group b) covers that order's k 32 b .. + 31;
+// block-scaled kernels (HWK) therefore load the fragment in that order.
+template <bool KC, bool HWK = false>
 __device__ __forceinline__ v8i read_frag(const uint8_t* lds, int base, int lane) {
   v8i f;
   if (KC) {
     const int r = base + (lane & 15);
     const int g = lane >> 4;
     const int s = swz_kc(r);
-    const v4i lo = *(const v4i*)(lds + r * 128 + (((2 * g) ^ s) * 16));
-    const v4i hi = *(const v4i*)(lds + r * 128 + (((2 * g + 1) ^ s) * 16));
+    const int c0 = HWK ? g : 2 * g, c1 = HWK ? 4 + g : 2 * g + 1;  // 16-byte k chunks
+    const v4i lo = *(const v4i*)(lds + r * 128 + ((c0 ^ s) * 16));
+    const v4i hi = *(const v4i*)(lds + r * 128 + ((c1 ^ s) * 16));
     f = v8i{lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
   } else {
     const int t = lane & 15, g = lane >> 4;
     const int cn = base >> 4;
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-      const int k = 32 * g + 8 * s + (t >> 1);
+      const int k = (HWK ? 64 * (s >> 1) + 16 * g + 8 * (s & 1) : 32 * g + 8 * s) + (t >> 1);
       const int off = k * 256 + ((cn ^ swz_mc(k)) * 16) + (t & 1) * 8;
       const v2i v = __builtin_amdgcn_ds_read_tr8_b64_v2i32((LDS_AS v2i*)(lds + off));
       f[2 * s] = v.x;
@@ -231,6 +251,19 @@ __device__ __forceinline__ v4f mfma(const v8i& bfrag, const v8i& afrag, const v4
   // First operand = B fragment (rows of the MFMA result index N), second =
   // A fragment: result lane l holds C[m = l & 15][n = 4 * (l >> 4) + i].
   return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(bfrag, afrag, c, FB, FA, 0, 0, 0, 0);
+}
+
+// The same MFMA with MX block scales: lane l's E8M0 bytes (byte 0 of sb, sa)
+// scale k-block l >> 4 of the step (k 32 (l >> 4) .. + 31 in the MFMA's k
+// order, which read_frag<..., true> makes the matrix's own) of B column / A
+// row (l & 15); 127 is a factor of 1.
+template <int FA, int FB, bool MX>
+__device__ __forceinline__ v4f mfma_s(const v8i& bfrag, const v8i& afrag, const v4f& c, int sb,
+                                      int sa) {
+  if constexpr (MX)
+    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(bfrag, afrag, c, FB, FA, 0, sb, 0, sa);
+  else
+    return mfma<FA, FB>(bfrag, afrag, c);
 }
 
 // One LDS read S of a fragment (read_frag split into its instructions, so
@@ -611,10 +644,13 @@ __device__ __forceinline__ void activate(v4f (&acc)[MI_][NI_], int e_w) {
 
 // CH: the fused epilogue also applies channel scales (instantiated apart, so
 // that the other fused kernels keep their register allocation).
-template <bool A_MN, bool B_KC, int FA, int FB, int EPI, bool FUSE, int NW, bool CH = false>
+template <bool A_MN, bool B_KC, int FA, int FB, int EPI, bool FUSE, int NW, bool CH = false,
+          bool MX = false>
 __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
   static_assert(NW == 8 || (NW == 4 && !FUSE), "the fused epilogue runs on the 8-wave kernel");
   static_assert(FUSE || !CH, "channel scales are part of the fused epilogue");
+  static_assert(!MX || (NW == 8 && !FUSE && EPI != EPI_INTER16),
+                "block scales: 8-wave kernel, plain epilogue, fp32 intermediate or direct cast");
   using C = WaveCfg<NW>;
   constexpr int WAVES = C::WAVES, WAVES_N = C::WAVES_N, WTM = C::WTM, WTN = C::WTN;
   constexpr int MI = C::MI, NI = C::NI, BPW = C::BPW, LOADS_PER_STEP = C::LOADS_PER_STEP;
@@ -671,6 +707,36 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
     __syncthreads();
   };
 
+  // MX block scales: per k-step, the 4 E8M0 bytes of every tile row of A
+  // and tile column of B (one dword of the [rows][mx_ld] arrays) are staged
+  // in LDS beside the step's tiles, one load per wave: wave w < 4 loads A
+  // rows 64 w .. 64 w + 63, wave w >= 4 B columns 64 (w - 4) .. (row r of
+  // the stage at byte 4 r; rows past M or N read zeros). Stage layout:
+  // [2 k-step stages][A 1 KiB | B 1 KiB].
+  uint8_t* sS = nullptr;
+  if constexpr (MX) {
+    __shared__ __attribute__((aligned(1024))) uint8_t s_mx[4096];
+    sS = s_mx;
+  }
+  const int KB = (K + 31) / 32;  // k-blocks holding data
+  auto issue_scales = [&](int kt, int stage) {
+    if constexpr (MX) {
+      const bool is_b = wave >= 4;
+      const int row = (is_b ? n0 : m0) + 64 * (wave & 3) + lane;
+      const v4i r = is_b ? make_rsrc(p.mx_b, p.mx_b_bytes) : make_rsrc(p.mx_a, p.mx_a_bytes);
+      const uint32_t off =
+          row < (is_b ? N : M) ? (uint32_t)row * p.mx_ld + 4u * (uint32_t)kt : (uint32_t)r.z;
+      load_lds4(r, off, sS + stage * 2048 + (is_b ? 1024 : 0) + 256 * (wave & 3));
+    }
+  };
+  // This lane's byte (k-block lane >> 4 of step kt) for tile row / column
+  // rc of operand half (0 A, 1 B); padding blocks past K count as 1.
+  auto scale_byte = [&](int stage, int half, int rc, int kt) -> int {
+    const int g = lane >> 4;
+    const int v = sS[stage * 2048 + half * 1024 + 4 * rc + g];
+    return 4 * kt + g < KB ? v : 127;
+  };
+
   v4f acc[MI][NI];  // NW = 8 (NW = 4: AccTile)
   if constexpr (NW == 8) {
 #pragma unroll
@@ -693,6 +759,8 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
   if constexpr (NW == 8) {
     v8i a[MI];   // A fragments of the step
     v8i bq[3];   // B fragments: in use and up to two groups ahead
+    int sa[MI] = {}, sb[NI] = {};  // MX: this lane's block-scale bytes of the step
+    const int r16 = lane & 15;
 
     // One k-step. LOADS: issue the loads of step kt + 2 into this step's
     // stage after the barrier. NEXT: step kt + 1 exists (barrier, then its A
@@ -708,9 +776,10 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
       // B column groups 0 .. NI - 3, fragments read two groups ahead
       static_for<0, NI - 2>([&](auto I) {
         constexpr int ni = decltype(I)::value;
-        bq[(ni + 2) % 3] = read_frag<B_KC>(cB, wn + 16 * (ni + 2), lane);
+        bq[(ni + 2) % 3] = read_frag<B_KC, MX>(cB, wn + 16 * (ni + 2), lane);
 #pragma unroll
-        for (int mi = 0; mi < MI; ++mi) acc[mi][ni] = mfma<FA, FB>(bq[ni % 3], a[mi], acc[mi][ni]);
+        for (int mi = 0; mi < MI; ++mi)
+          acc[mi][ni] = mfma_s<FA, FB, MX>(bq[ni % 3], a[mi], acc[mi][ni], sb[ni], sa[mi]);
 #pragma unroll
         for (int mi = 0; mi < MI; ++mi) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
@@ -727,45 +796,72 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
         __syncthreads();
         __builtin_amdgcn_sched_barrier(0);
         if (!LOADS && kt + 1 == KT_full && (krem & 15)) zero_tail(nA, nB);
+        // MX: B column groups 0 .. NI - 3 are done with their bytes
+        if constexpr (MX) {
+#pragma unroll
+          for (int ni = 0; ni < NI - 2; ++ni) sb[ni] = scale_byte(!odd, 1, wn + 16 * ni + r16, kt + 1);
+        }
       }
       // B column groups NI - 2 and NI - 1, taken row block by row block: once
       // both MFMAs of a[mi] have issued, a[mi] is refilled with the fragment
       // of step kt + 1; the loads of step kt + 2 go out two per row block.
 #pragma unroll
       for (int mi = 0; mi < MI; ++mi) {
-        acc[mi][NI - 2] = mfma<FA, FB>(bq[(NI - 2) % 3], a[mi], acc[mi][NI - 2]);
-        acc[mi][NI - 1] = mfma<FA, FB>(bq[(NI - 1) % 3], a[mi], acc[mi][NI - 1]);
+        acc[mi][NI - 2] =
+            mfma_s<FA, FB, MX>(bq[(NI - 2) % 3], a[mi], acc[mi][NI - 2], sb[NI - 2], sa[mi]);
+        acc[mi][NI - 1] =
+            mfma_s<FA, FB, MX>(bq[(NI - 1) % 3], a[mi], acc[mi][NI - 1], sb[NI - 1], sa[mi]);
         if (LOADS) {
           issue_one(2 * mi, kt + 2, cA, cB);
           issue_one(2 * mi + 1, kt + 2, cA, cB);
+          if (mi == MI - 1) issue_scales(kt + 2, odd);
         }
-        if (NEXT) a[mi] = read_frag<!A_MN>(nA, wm + 16 * mi, lane);
+        if (NEXT) {
+          a[mi] = read_frag<!A_MN, MX>(nA, wm + 16 * mi, lane);
+          if constexpr (MX) sa[mi] = scale_byte(!odd, 0, wm + 16 * mi + r16, kt + 1);
+        }
       }
       if (NEXT) {
-        bq[0] = read_frag<B_KC>(nB, wn, lane);
-        bq[1] = read_frag<B_KC>(nB, wn + 16, lane);
+        bq[0] = read_frag<B_KC, MX>(nB, wn, lane);
+        bq[1] = read_frag<B_KC, MX>(nB, wn + 16, lane);
+        if constexpr (MX) {
+          sb[NI - 2] = scale_byte(!odd, 1, wn + 16 * (NI - 2) + r16, kt + 1);
+          sb[NI - 1] = scale_byte(!odd, 1, wn + 16 * (NI - 1) + r16, kt + 1);
+        }
       }
       static_for<0, MI>([&](auto I) {
         constexpr int i = decltype(I)::value;
+        // MX: the B bytes after the barrier, one A byte per row block, the
+        // last two B bytes at the end
+        constexpr int XS = MX ? 1 + (i == 0 ? NI - 2 : 0) + (i + 1 == MI ? 2 : 0) : 0;
         __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-        if (NEXT) __builtin_amdgcn_sched_group_barrier(0x100, i + 1 < MI ? DSA : DSA + 2 * DSB, 0);
+        if (NEXT)
+          __builtin_amdgcn_sched_group_barrier(0x100, (i + 1 < MI ? DSA : DSA + 2 * DSB) + XS, 0);
       });
     };
 
     if (KT > 0) {
       issue_all(0, sA0, sB0);
+      issue_scales(0, 0);
       if (KT > 1) {
         issue_all(1, sA1, sB1);
-        wait_vmcnt<LOADS_PER_STEP>();
+        issue_scales(1, 1);
+        wait_vmcnt<LOADS_PER_STEP + (MX ? 1 : 0)>();  // step 1's loads may be in flight
       } else {
         wait_vmcnt<0>();
       }
       __syncthreads();
       if (KT_full == 0 && (krem & 15)) zero_tail(sA0, sB0);
 #pragma unroll
-      for (int mi = 0; mi < MI; ++mi) a[mi] = read_frag<!A_MN>(sA0, wm + 16 * mi, lane);
-      bq[0] = read_frag<B_KC>(sB0, wn, lane);
-      bq[1] = read_frag<B_KC>(sB0, wn + 16, lane);
+      for (int mi = 0; mi < MI; ++mi) a[mi] = read_frag<!A_MN, MX>(sA0, wm + 16 * mi, lane);
+      bq[0] = read_frag<B_KC, MX>(sB0, wn, lane);
+      bq[1] = read_frag<B_KC, MX>(sB0, wn + 16, lane);
+      if constexpr (MX) {
+#pragma unroll
+        for (int mi = 0; mi < MI; ++mi) sa[mi] = scale_byte(0, 0, wm + 16 * mi + r16, 0);
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni) sb[ni] = scale_byte(0, 1, wn + 16 * ni + r16, 0);
+      }
     }
     int kt = 0;
     for (; kt + 2 < KT; ++kt) step(T_{}, T_{}, kt);
@@ -876,9 +972,9 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
       __syncthreads();
       if (KT_full == 0 && (krem & 15)) zero_tail(sA0, sB0);
 #pragma unroll
-      for (int mi = 0; mi < MI; ++mi) af[0][mi] = read_frag<!A_MN>(sA0, wm + 16 * mi, lane);
-      bf[0] = read_frag<B_KC>(sB0, wn, lane);
-      bf[1] = read_frag<B_KC>(sB0, wn + 16, lane);
+      for (int mi = 0; mi < MI; ++mi) af[0][mi] = read_frag<!A_MN, MX>(sA0, wm + 16 * mi, lane);
+      bf[0] = read_frag<B_KC, MX>(sB0, wn, lane);
+      bf[1] = read_frag<B_KC, MX>(sB0, wn + 16, lane);
       using P0 = std::integral_constant<int, 0>;
       using P1 = std::integral_constant<int, 1>;
       head(P0{}, 0);
@@ -901,8 +997,10 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
   const int nb = n0 + wn + 4 * (lane >> 4);
   // EPI_DIRECT: data' = acc * 2^-shift, shift from the prologue
   const int shift = EPI == EPI_DIRECT ? (int)__builtin_amdgcn_readfirstlane(p.hdr[2]) : 0;
-  // Fused values may be fp32 subnormals (the accumulators never are).
-  const bool fast = shift >= (FUSE ? kFastShiftMinSub : -kFastShiftMax) && shift <= kFastShiftMax;
+  // Fused values and block-scaled accumulators may be fp32 subnormals (the
+  // plain accumulators never are).
+  const bool fast =
+      shift >= ((FUSE || MX) ? kFastShiftMinSub : -kFastShiftMax) && shift <= kFastShiftMax;
   const float hw_scale = fast ? pow2_float(shift) : 1.0f;
   const float hw_inv = fast ? pow2_float(-shift) : 1.0f;
   const bool sat = p.sat != 0;
@@ -1117,6 +1215,32 @@ hipError_t launch_fmt(const GemmParams& p, int epi, hipStream_t s) {
     default:
       return launch_epi<A_MN, B_KC, FUSE, FA, FB, EPI_DIRECT>(p, s);
   }
+}
+
+// MX block scales: the 8-wave kernel with the fp32 intermediate (NONE,
+// AMAX) or the direct cast (DELAYED); one source file per layout
+// (gemm_<layout>_mx.hip).
+template <bool A_MN, bool B_KC>
+hipError_t launch_layout_mx(const GemmParams& p, int fa, int fb, int epi, hipStream_t s);
+
+template <bool A_MN, bool B_KC, int FA, int FB>
+hipError_t launch_mx(const GemmParams& p, int epi, hipStream_t s) {
+  const dim3 grid(p.tiles_m * p.tiles_n), block(WaveCfg<8>::NTHR);
+  if (epi == EPI_DIRECT)
+    hipLaunchKernelGGL((gemm_kernel<A_MN, B_KC, FA, FB, EPI_DIRECT, false, 8, false, true>), grid,
+                       block, 0, s, p);
+  else
+    hipLaunchKernelGGL((gemm_kernel<A_MN, B_KC, FA, FB, EPI_INTER32, false, 8, false, true>), grid,
+                       block, 0, s, p);
+  return hipGetLastError();
+}
+
+template <bool A_MN, bool B_KC>
+hipError_t launch_formats_mx(const GemmParams& p, int fa, int fb, int epi, hipStream_t s) {
+  if (fa == kE4M3 && fb == kE4M3) return launch_mx<A_MN, B_KC, kE4M3, kE4M3>(p, epi, s);
+  if (fa == kE4M3 && fb == kE5M2) return launch_mx<A_MN, B_KC, kE4M3, kE5M2>(p, epi, s);
+  if (fa == kE5M2 && fb == kE4M3) return launch_mx<A_MN, B_KC, kE5M2, kE4M3>(p, epi, s);
+  return launch_mx<A_MN, B_KC, kE5M2, kE5M2>(p, epi, s);
 }
 
 template <bool A_MN, bool B_KC, bool FUSE>

@@ -1,0 +1,13 @@
+// Instantiations of the scaled FP8 GEMM with MX block scales for A stored
+// [M][K] and B stored [K][N].
+#include "gemm_kernel.h"
+
+namespace scalify {
+
+template <>
+hipError_t launch_layout_mx<false, false>(const GemmParams& p, int fa, int fb, int epi,
+                                        hipStream_t s) {
+  return launch_formats_mx<false, false>(p, fa, fb, epi, s);
+}
+
+}  // namespace scalify

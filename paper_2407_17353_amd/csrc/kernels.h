@@ -54,6 +54,12 @@ struct GemmParams {
   // accumulator with the power-of-two product of the epilogue; NULL = 1.
   const float* ch_a;
   const float* ch_b;
+  // MX block scales (MX kernels only): E8M0 bytes [M][mx_ld] for A and
+  // [N][mx_ld] for B, byte k / 32 of a row scaling that row's k; mx_ld =
+  // 4 * ceil(K / 128); byte sizes of the arrays for the buffer range checks.
+  const uint8_t* mx_a;
+  const uint8_t* mx_b;
+  uint32_t mx_ld, mx_a_bytes, mx_b_bytes;
 };
 
 // fuse: launch the kernels with the fused residual add / activation / pre_out

@@ -52,6 +52,14 @@ bool is_fused(const scalify_matmul_opts* o) {
          o->a_channel_scale != nullptr || o->b_channel_scale != nullptr;
 }
 
+bool has_mx(const scalify_matmul_opts* o) {
+  return o->a_block_scale != nullptr || o->b_block_scale != nullptr;
+}
+
+// Calls whose pre-cast value may be any fp32 (fused epilogues, block
+// scales) keep an fp32 intermediate.
+bool f32_intermediate(const scalify_matmul_opts* o) { return is_fused(o) || has_mx(o); }
+
 // Residual of the fused scaled add: M x N, row-major, ld = 0 (one row for
 // every row) or ld >= N; the very same matrix as out, or disjoint from it.
 scalify_status check_residual(const scalify_scaled_array* r, const scalify_scaled_array* out,
@@ -128,6 +136,8 @@ size_t layernorm_bwd_ws(int64_t R, int64_t D) {
 
 extern "C" {
 
+int64_t scalify_mx_block_scale_ld(int64_t K) { return K < 1 ? 0 : 4 * ((K + 127) / 128); }
+
 int32_t scalify_matmul_scale_log2(int64_t K) {
   // Largest e with 2^e <= sqrt(K), i.e. 4^e <= K (integer arithmetic only).
   int32_t e = 0;
@@ -142,7 +152,7 @@ size_t scalify_matmul_workspace_size(int64_t M, int64_t N, int32_t out_dtype, in
 
 size_t scalify_matmul_workspace_size_opts(int64_t M, int64_t N, const scalify_matmul_opts* opts) {
   if (!opts) return 0;
-  return matmul_ws(M, N, opts->out_dtype, opts->rescale, is_fused(opts));
+  return matmul_ws(M, N, opts->out_dtype, opts->rescale, f32_intermediate(opts));
 }
 
 size_t scalify_rescale_workspace_size(int64_t n) { return n < 0 ? 0 : kHeaderBytes; }
@@ -188,11 +198,22 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
   if (!aligned16(opts->b_channel_scale) || ((uintptr_t)opts->a_channel_scale & 3u))
     return SCALIFY_ERR_ALIGN;
   const bool fused = is_fused(opts);
+  const bool mx = has_mx(opts);
+  const int64_t mx_ld = scalify_mx_block_scale_ld(K);
+  if (mx) {
+    // an array of no bytes (M, N or K zero) may be NULL
+    if ((!opts->a_block_scale && M * K > 0) || (!opts->b_block_scale && N * K > 0))
+      return SCALIFY_ERR_NULL;
+    if (fused) return SCALIFY_ERR_VALUE;
+    if (((uintptr_t)opts->a_block_scale | (uintptr_t)opts->b_block_scale) & 3u)
+      return SCALIFY_ERR_ALIGN;
+    if (M * mx_ld >= ((int64_t)1 << 32) || N * mx_ld >= ((int64_t)1 << 32)) return SCALIFY_ERR_SHAPE;
+  }
   // 32-bit byte offsets inside the GEMM kernel, including the range-checked
   // reads of up to one tile past the last stored row.
   if (M && K && (stored_rows(a) + 256) * a->ld + 256 >= ((int64_t)1 << 32)) return SCALIFY_ERR_SHAPE;
   if (K && N && (stored_rows(b) + 256) * b->ld + 256 >= ((int64_t)1 << 32)) return SCALIFY_ERR_SHAPE;
-  const size_t need = matmul_ws(M, N, opts->out_dtype, opts->rescale, fused);
+  const size_t need = matmul_ws(M, N, opts->out_dtype, opts->rescale, fused || mx);
   if (!workspace || workspace_bytes < need || ((uintptr_t)workspace & 255u))
     return SCALIFY_ERR_WORKSPACE;
 
@@ -204,9 +225,12 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
   // Delayed: the output scale comes from the statistic of an earlier call,
   // so the GEMM casts straight to codes (no intermediate). Otherwise the GEMM
   // writes a pre-cast intermediate: 16-bit for FP8 outputs of the plain
-  // epilogue, fp32 for FP16 outputs and for fused epilogues.
+  // epilogue, fp32 for FP16 outputs, for fused epilogues and with block
+  // scales (whose accumulators may be fp32 subnormals, which the 16-bit
+  // encoding does not keep exactly).
   const int epi = delayed ? EPI_DIRECT
-                          : ((opts->out_dtype == SCALIFY_F16 || fused) ? EPI_INTER32 : EPI_INTER16);
+                          : ((opts->out_dtype == SCALIFY_F16 || fused || mx) ? EPI_INTER32
+                                                                              : EPI_INTER16);
   // Exponent offset of the statistic: the matmul data is acc * 2^-e_c; with
   // a residual the statistic is taken over w itself.
   const int e_cc = res ? 0 : e_c;
@@ -251,6 +275,12 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
   p.pre_out = opts->pre_out;
   p.ch_a = opts->a_channel_scale;
   p.ch_b = opts->b_channel_scale;
+  // (the block-scale kernels run whenever the product has terms: K > 0)
+  p.mx_a = mx && K > 0 ? opts->a_block_scale : nullptr;
+  p.mx_b = mx && K > 0 ? opts->b_block_scale : nullptr;
+  p.mx_ld = (uint32_t)mx_ld;
+  p.mx_a_bytes = (uint32_t)(M * mx_ld);
+  p.mx_b_bytes = (uint32_t)(N * mx_ld);
   hipEvent_t* ev = (hipEvent_t*)opts->events;
   if (ev && ev[0] && hipEventRecord(ev[0], s) != hipSuccess) return SCALIFY_ERR_HIP;
   if (M > 0 && N > 0) {

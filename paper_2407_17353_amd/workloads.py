@@ -58,6 +58,15 @@ def int_grid(shape, fmt: int, seed: int, device="cpu", vmax: int = 8):
     return v.to(_TORCH_FP8[fmt]).view(torch.uint8)
 
 
+def mx_block_scales(rows: int, K: int, seed: int, lo: int = -8, hi: int = 8, device="cpu"):
+    """E8M0 block-scale bytes [rows][4 * ceil(K / 128)] (one per 32 k,
+    padded to whole 128-k steps): 127 + an exponent uniform in [lo, hi], the
+    spread of per-block scales of FP8 data quantized block by block."""
+    ld = 4 * ((K + 127) // 128)
+    e = torch.randint(lo, hi + 1, (rows, ld), generator=_gen(seed, "cpu"), dtype=torch.int32)
+    return (e + 127).to(torch.uint8).to(device)
+
+
 def scale_log2_draw(seed: int, lo: int, hi: int) -> int:
     g = _gen(seed, "cpu")
     return int(torch.randint(lo, hi + 1, (1,), generator=g).item())

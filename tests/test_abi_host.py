@@ -78,6 +78,8 @@ def call_matmul(a, b, out, opts=None, ws=FAKE + 8192, ws_bytes=1 << 40):
     ("negative", 3), ("ld_small", 3), ("ld_unaligned", 5), ("ptr_unaligned", 5),
     ("ws_small", 6), ("ws_null", 6), ("ws_unaligned", 6), ("null_data", 1), ("too_big", 3),
     ("channel_b_unaligned", 5), ("channel_a_unaligned", 5),
+    ("mx_a_only", 1), ("mx_b_only", 1), ("mx_unaligned", 5), ("mx_with_activation", 7),
+    ("mx_with_channel", 7),
 ])
 def test_matmul_argument_errors(case, status):
     a, b, out = arr(64, 128), arr(128, 32), arr(64, 32)
@@ -127,6 +129,17 @@ def test_matmul_argument_errors(case, status):
     elif case == "channel_a_unaligned":
         o = sc.CMatmulOpts(sc.E4M3, 1, 0, 1)
         o.a_channel_scale = FAKE + 2
+        kw["opts"] = o
+    elif case.startswith("mx_"):
+        o = sc.CMatmulOpts(sc.E4M3, 1, 0, 1)
+        o.a_block_scale = None if case == "mx_b_only" else FAKE + 65536
+        o.b_block_scale = None if case == "mx_a_only" else FAKE + 131072
+        if case == "mx_unaligned":
+            o.b_block_scale = FAKE + 131072 + 2
+        elif case == "mx_with_activation":
+            o.activation = sc.ACT_RELU
+        elif case == "mx_with_channel":
+            o.a_channel_scale = FAKE + 196608
         kw["opts"] = o
     assert call_matmul(a, b, out, **kw) == status
 
@@ -181,7 +194,21 @@ def test_fused_workspace_sizes():
     o = sc.CMatmulOpts(sc.E4M3, sc.RESCALE_AMAX, 0, 1)
     o.b_channel_scale = FAKE
     assert sc.load_library().scalify_matmul_workspace_size_opts(10, 10, ctypes.byref(o)) == 256 + 10 * 16 * 4
+    # so do MX block scales
+    o = sc.CMatmulOpts(sc.E4M3, sc.RESCALE_AMAX, 0, 1)
+    o.a_block_scale, o.b_block_scale = FAKE, FAKE + 4096
+    assert sc.load_library().scalify_matmul_workspace_size_opts(10, 10, ctypes.byref(o)) == 256 + 10 * 16 * 4
     assert sc.load_library().scalify_matmul_workspace_size_opts(10, 10, None) == 0
+
+
+def test_mx_block_scale_row_length():
+    """One byte per 32 k, padded to whole 128-k steps; the oracle's helper
+    states the same layout independently."""
+    from oracle import oracle as orc
+    for K in (1, 31, 32, 33, 127, 128, 129, 200, 8192, 11008):
+        assert sc.scalify_mx_block_scale_ld(K) == 4 * ((K + 127) // 128) == orc.mx_block_scale_ld(K)
+        assert sc.scalify_mx_block_scale_ld(K) >= (K + 31) // 32
+    assert sc.scalify_mx_block_scale_ld(0) == 0
 
 
 def fused_opts(residual=None, act=sc.ACT_NONE, pre_out=None, out_dtype=sc.E4M3,
