@@ -89,7 +89,8 @@ def copy_calibration(dev, nbytes=256 << 20, reps=5):
     del src, dst
 
 
-def time_case(case, steps, warmup, dev, ws=None, mode=None, act=0, residual_seed=None):
+def time_case(case, steps, warmup, dev, ws=None, mode=None, act=0, residual_seed=None,
+              mx_seed=None):
     """Time `steps` scalify_matmul calls of one GemmCase. Returns a dict with
     ms per call (event-timed over the whole timed region), the mean and the
     p10/p50/p90 duration of the fused GEMM kernel (events recorded by the
@@ -102,7 +103,8 @@ def time_case(case, steps, warmup, dev, ws=None, mode=None, act=0, residual_seed
     one device word that every call reads and rewrites (model state).
     act / residual_seed: fuse that activation and, when residual_seed is
     given, the scaled add of a seeded E4M3 N(0,1) residual [M, N] (scale 2)
-    into the GEMM epilogue."""
+    into the GEMM epilogue. mx_seed: give A and B seeded MX block scales
+    (E8M0 bytes per 32 k, exponents in [-8, 8])."""
     import torch
     from paper_2407_17353_amd import binding as sc
 
@@ -113,7 +115,9 @@ def time_case(case, steps, warmup, dev, ws=None, mode=None, act=0, residual_seed
     b = sc.ScaledArray(B, case.fb, sc.scale_tensor(case.b_scale_log2, dev), case.tb)
     out = sc.empty_scaled(case.M, case.N, case.fout, dev)
     fused = act != 0 or residual_seed is not None
-    need = sc.scalify_matmul_workspace_size_opts(case.M, case.N, case.fout, mode, fused)
+    # block scales keep the fp32 intermediate of the fused calls
+    need = sc.scalify_matmul_workspace_size_opts(case.M, case.N, case.fout, mode,
+                                                 fused or mx_seed is not None)
     if ws is None or ws.numel() < need:
         ws = sc.workspace(need, dev)
     state = torch.zeros(1, dtype=torch.float32, device=dev)
@@ -124,6 +128,10 @@ def time_case(case, steps, warmup, dev, ws=None, mode=None, act=0, residual_seed
         from paper_2407_17353_amd import workloads as wl
         R = wl.fp8_normal((case.M, case.N), wl.E4M3, residual_seed, dev)
         kw["residual"] = sc.ScaledArray(R, wl.E4M3, sc.scale_tensor(1, dev))
+    if mx_seed is not None:
+        from paper_2407_17353_amd import workloads as wl
+        kw["a_block_scale"] = wl.mx_block_scales(case.M, case.K, mx_seed, device=dev)
+        kw["b_block_scale"] = wl.mx_block_scales(case.N, case.K, mx_seed + 1, device=dev)
     stream = torch.cuda.current_stream()
     for _ in range(warmup):
         sc.scalify_matmul(a, b, out, rescale=mode, ws=ws, **kw)
@@ -308,6 +316,17 @@ def main():
             "ms_per_step": round(rf["ms_per_step"], 4),
             "gemm_kernel_us": round(rf["gemm_ms"] * 1e3, 2),
             "epilogue_cast_us": round(rf["cast_ms"] * 1e3, 2) if m == sc.RESCALE_AMAX else None}
+    # The same workload with MX block scales (Section 2: block-scaling formats
+    # as scales broadcastable to the data), applied by the scaled MFMA.
+    line["mx_block_scales"] = {}
+    for name, m in (("amax", sc.RESCALE_AMAX), ("delayed", sc.RESCALE_DELAYED)):
+        rm, ws = time_case(case, args.steps // 2, args.warmup // 2, dev, ws, mode=m,
+                           mx_seed=wl.seed_of(4, 40))
+        line["mx_block_scales"][name] = {
+            "value": round(flops / (rm["ms_per_step"] * 1e-3) / 1e12, 2), "unit": "TFLOP/s",
+            "ms_per_step": round(rm["ms_per_step"], 4),
+            "gemm_kernel_us": round(rm["gemm_ms"] * 1e3, 2),
+            "epilogue_cast_us": round(rm["cast_ms"] * 1e3, 2) if m == sc.RESCALE_AMAX else None}
     line["layernorm"] = time_layernorm(dev, 20, 10)
     if args.sweep:
         sweep = []
