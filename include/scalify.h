@@ -134,19 +134,37 @@ typedef struct {
                             16-byte aligned; NULL = none */
     const uint8_t* a_block_scale; /* optional MX block scales of a (Section 2: block
                             scaling formats such as MX as scales broadcastable to the
-                            data): device E8M0 bytes [M][scalify_mx_block_scale_ld(K)],
-                            byte a_block_scale[i * ld + k / 32] (value 2^(byte - 127))
-                            scaling a[i,k] on top of *a.scale; 4-byte aligned; given
-                            together with b_block_scale; NULL = none */
-    const uint8_t* b_block_scale; /* device E8M0 bytes [N][scalify_mx_block_scale_ld(K)],
-                            byte b_block_scale[j * ld + k / 32] scaling b[k,j] (per column
-                            of the logical b); 4-byte aligned; NULL = none */
+                            data): P, one E8M0 byte P[i][k / 32] (value 2^(byte - 127))
+                            per 32 k of each row i of the logical a, scaling a[i,k] on
+                            top of *a.scale, in the packed order that
+                            scalify_mx_pack_block_scales writes (rows = M); device,
+                            4-byte aligned; given together with b_block_scale;
+                            NULL = none */
+    const uint8_t* b_block_scale; /* Q, one byte Q[j][k / 32] per 32 k of each column j
+                            of the logical b, packed likewise (rows = N); NULL = none */
 } scalify_matmul_opts;
 
-/* Row length in bytes of an MX block-scale array for depth K: one byte per
- * 32 k, padded to whole 128-k steps, 4 * ceil(K / 128). Bytes of a row at
- * k / 32 >= ceil(K / 32) are padding, never used. Returns 0 for K < 1. */
-int64_t scalify_mx_block_scale_ld(int64_t K);
+/* Bytes of the packed form of an MX block-scale array with `rows` rows (rows
+ * of a, or columns of b) for depth K: 256 * ceil(K / 128) * ceil(rows / 64).
+ * Returns 0 when rows or K is below 1. */
+int64_t scalify_mx_packed_bytes(int64_t rows, int64_t K);
+
+/* Pack MX block-scale bytes from the natural row-major order, src[r * src_ld
+ * + b] for row r < rows and block b < ceil(K / 32) (src_ld >= ceil(K / 32)),
+ * into the order the block-scaled matmul reads: for 128-k step t, 64-row
+ * group q, k-block g in 0..3 and row r in 0..15 of the group's four 16-row
+ * blocks, the 4 bytes of rows 64 q + r, + 16, + 32, + 48 at block 4 t + g
+ * are the 32-bit word at byte offset ((t * ceil(rows / 64) + q) * 64 + 16 g
+ * + r) * 4 of dst (lowest byte first). Blocks past ceil(K / 32) and rows
+ * past `rows` are written as 127 (a factor of 1; they meet zero data).
+ * dst: device, scalify_mx_packed_bytes(rows, K) bytes, 4-byte aligned,
+ * not overlapping src. Pure data movement; enqueued on `stream`. Weights'
+ * scales are packed once; an activation's producer can write this order
+ * directly. Errors: SCALIFY_ERR_NULL (NULL src or dst with rows, K > 0),
+ * SCALIFY_ERR_SHAPE (negative sizes, src_ld < ceil(K / 32), more than 2^32
+ * bytes), SCALIFY_ERR_ALIGN (dst), SCALIFY_ERR_HIP. */
+scalify_status scalify_mx_pack_block_scales(const uint8_t* src, int64_t rows, int64_t K,
+                                            int64_t src_ld, uint8_t* dst, void* stream);
 
 /* Exponent e_c of the matmul scale rule (Section 3.2, Algorithm 3): the
  * largest e with 2^e <= sqrt(K) (sqrt(K) rounded down to a power of two),
@@ -195,7 +213,7 @@ size_t scalify_matmul_workspace_size_opts(int64_t M, int64_t N, const scalify_ma
  * keeps an fp32 intermediate like a fused one.
  *
  * MX block scales (opts.a_block_scale = P, opts.b_block_scale = Q, both or
- * neither): a[i,k] = dec(a)[i,k] * s_a * 2^(P[i][k/32] - 127), b[k,j] =
+ * neither, each packed by scalify_mx_pack_block_scales): a[i,k] = dec(a)[i,k] * s_a * 2^(P[i][k/32] - 127), b[k,j] =
  * dec(b)[k,j] * s_b * 2^(Q[j][k/32] - 127): the matrix cores apply the block
  * factors to the products, acc = sum_k dec(a)[i,k] dec(b)[k,j]
  * 2^(P[i][k/32] + Q[j][k/32] - 254), and everything below acts on that acc

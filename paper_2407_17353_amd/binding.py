@@ -58,7 +58,7 @@ EXPORTED = ("scalify_matmul_scale_log2", "scalify_matmul_workspace_size",
             "scalify_rescale_workspace_size", "scalify_rescale", "scalify_cast",
             "scalify_set_scaling", "scalify_status_string", "scalify_layernorm_fwd",
             "scalify_layernorm_bwd_workspace_size", "scalify_layernorm_bwd",
-            "scalify_mx_block_scale_ld")
+            "scalify_mx_packed_bytes", "scalify_mx_pack_block_scales")
 
 _lib = None
 
@@ -76,8 +76,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
     lib.scalify_matmul_scale_log2.argtypes = [i64]
     lib.scalify_matmul_scale_log2.restype = i32
-    lib.scalify_mx_block_scale_ld.argtypes = [i64]
-    lib.scalify_mx_block_scale_ld.restype = i64
+    lib.scalify_mx_packed_bytes.argtypes = [i64, i64]
+    lib.scalify_mx_packed_bytes.restype = i64
+    lib.scalify_mx_pack_block_scales.argtypes = [vp, i64, i64, i64, vp, vp]
+    lib.scalify_mx_pack_block_scales.restype = ctypes.c_int
     lib.scalify_matmul_workspace_size.argtypes = [i64, i64, i32, i32]
     lib.scalify_matmul_workspace_size.restype = ctypes.c_size_t
     lib.scalify_matmul_workspace_size_opts.argtypes = [i64, i64, P(CMatmulOpts)]
@@ -157,9 +159,25 @@ def scalify_matmul_scale_log2(K: int) -> int:
     return int(load_library().scalify_matmul_scale_log2(int(K)))
 
 
-def scalify_mx_block_scale_ld(K: int) -> int:
-    """Row length (bytes) of an MX block-scale array for depth K."""
-    return int(load_library().scalify_mx_block_scale_ld(int(K)))
+def scalify_mx_packed_bytes(rows: int, K: int) -> int:
+    """Bytes of the packed form of an MX block-scale array (rows x K)."""
+    return int(load_library().scalify_mx_packed_bytes(int(rows), int(K)))
+
+
+def scalify_mx_pack_block_scales(src: torch.Tensor, K: int, stream=None) -> torch.Tensor:
+    """Pack row-major E8M0 block-scale bytes src [rows, ld] (uint8 device
+    tensor, ld >= ceil(K / 32), byte [r, k // 32] scaling row r's k) into the
+    order scalify_matmul reads; returns a new uint8 device tensor."""
+    if src.dtype != torch.uint8 or src.dim() != 2 or src.stride(1) != 1:
+        raise ValueError("src: uint8 [rows, ld] with unit column stride")
+    rows = src.shape[0]
+    dst = torch.empty(max(scalify_mx_packed_bytes(rows, K), 4), dtype=torch.uint8,
+                      device=src.device)
+    st = load_library().scalify_mx_pack_block_scales(
+        src.data_ptr() if src.numel() else None, rows, int(K), src.stride(0), dst.data_ptr(),
+        _stream_handle(stream))
+    _check(st, "scalify_mx_pack_block_scales")
+    return dst[:scalify_mx_packed_bytes(rows, K)]
 
 
 def scalify_matmul_workspace_size(M: int, N: int, out_fmt: int, rescale: int = RESCALE_AMAX) -> int:
@@ -202,9 +220,9 @@ def scalify_matmul(a: ScaledArray, b: ScaledArray, out: ScaledArray, *, rescale:
     receives the pre-cast value w (validation). `a_channel_scale` /
     `b_channel_scale`: contiguous fp32 device tensors [M] / [N] of powers of
     two, channel scales of a's rows / b's columns. `a_block_scale` /
-    `b_block_scale`: uint8 device tensors [M, ld] / [N, ld] of E8M0 bytes,
-    ld = scalify_mx_block_scale_ld(K), MX block scales (one per 32 k) of
-    a's rows / b's columns.
+    `b_block_scale`: MX block scales (E8M0, one per 32 k) of a's rows / b's
+    columns, as returned by scalify_mx_pack_block_scales (uint8 device
+    tensors of scalify_mx_packed_bytes(M or N, K) bytes).
     `events`: an optional sequence of 3 torch.cuda.Event(enable_timing=True)
     recorded before the GEMM kernel, after it and after the epilogue (None
     entries are skipped)."""
@@ -229,8 +247,8 @@ def scalify_matmul(a: ScaledArray, b: ScaledArray, out: ScaledArray, *, rescale:
                        b_block_scale.data_ptr() if b_block_scale is not None else None)
     for t, rows in ((a_block_scale, M), (b_block_scale, N)):
         if t is not None and (t.dtype != torch.uint8 or not t.is_contiguous() or
-                              tuple(t.shape) != (rows, scalify_mx_block_scale_ld(a.shape[1]))):
-            raise ValueError("block scales: contiguous uint8 [rows, scalify_mx_block_scale_ld(K)]")
+                              t.numel() != scalify_mx_packed_bytes(rows, a.shape[1])):
+            raise ValueError("block scales: packed by scalify_mx_pack_block_scales")
     cr = residual.c_struct() if residual is not None else None
     if cr is not None:
         opts.residual = ctypes.pointer(cr)

@@ -24,4 +24,33 @@ hipError_t launch_gemm(const GemmParams& p, bool a_mn, bool b_kc, int fa, int fb
   return launch_layout<true, false, false>(p, fa, fb, epi, s);
 }
 
+// One thread per packed 32-bit word: word ((t * G + q) * 64 + 16 g + r)
+// holds, lowest byte first, the bytes of rows 64 q + r + 16 i (i = 0..3) at
+// k-block 4 t + g; rows and blocks outside the array read as 127 (factor 1).
+__global__ __launch_bounds__(256) void mx_pack_kernel(const uint8_t* __restrict__ src, int rows,
+                                                      int nblk, int ld, int groups, int words,
+                                                      uint32_t* __restrict__ dst) {
+  const int w = blockIdx.x * 256 + threadIdx.x;
+  if (w >= words) return;
+  const int lane = w & 63, q = (w >> 6) % groups, t = (w >> 6) / groups;
+  const int blk = 4 * t + (lane >> 4);
+  uint32_t v = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = 64 * q + 16 * i + (lane & 15);
+    const uint32_t byte = (r < rows && blk < nblk) ? src[(int64_t)r * ld + blk] : 127u;
+    v |= byte << (8 * i);
+  }
+  dst[w] = v;
+}
+
+hipError_t launch_mx_pack(const uint8_t* src, int rows, int K, int ld, uint8_t* dst,
+                          hipStream_t s) {
+  const int groups = (rows + 63) / 64, steps = (K + 127) / 128;
+  const int words = steps * groups * 64;
+  hipLaunchKernelGGL(mx_pack_kernel, dim3((words + 255) / 256), dim3(256), 0, s, src, rows,
+                     (K + 31) / 32, ld, groups, words, (uint32_t*)dst);
+  return hipGetLastError();
+}
+
 }  // namespace scalify

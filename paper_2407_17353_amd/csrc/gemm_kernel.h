@@ -253,15 +253,15 @@ __device__ __forceinline__ v4f mfma(const v8i& bfrag, const v8i& afrag, const v4
   return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(bfrag, afrag, c, FB, FA, 0, 0, 0, 0);
 }
 
-// The same MFMA with MX block scales: lane l's E8M0 bytes (byte 0 of sb, sa)
-// scale k-block l >> 4 of the step (k 32 (l >> 4) .. + 31 in the MFMA's k
-// order, which read_frag<..., true> makes the matrix's own) of B column / A
-// row (l & 15); 127 is a factor of 1.
-template <int FA, int FB, bool MX>
+// The same MFMA with MX block scales: byte SB of sb and byte SA of sa (E8M0,
+// 127 a factor of 1) scale k-block l >> 4 of the step (k 32 (l >> 4) .. + 31
+// in the MFMA's k order, which read_frag<..., true> makes the matrix's own)
+// of B column / A row (l & 15), for lane l.
+template <int FA, int FB, bool MX, int SB = 0, int SA = 0>
 __device__ __forceinline__ v4f mfma_s(const v8i& bfrag, const v8i& afrag, const v4f& c, int sb,
                                       int sa) {
   if constexpr (MX)
-    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(bfrag, afrag, c, FB, FA, 0, sb, 0, sa);
+    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(bfrag, afrag, c, FB, FA, SB, sb, SA, sa);
   else
     return mfma<FA, FB>(bfrag, afrag, c);
 }
@@ -707,34 +707,32 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
     __syncthreads();
   };
 
-  // MX block scales: per k-step, the 4 E8M0 bytes of every tile row of A
-  // and tile column of B (one dword of the [rows][mx_ld] arrays) are staged
-  // in LDS beside the step's tiles, one load per wave: wave w < 4 loads A
-  // rows 64 w .. 64 w + 63, wave w >= 4 B columns 64 (w - 4) .. (row r of
-  // the stage at byte 4 r; rows past M or N read zeros). Stage layout:
-  // [2 k-step stages][A 1 KiB | B 1 KiB].
+  // MX block scales, packed (see GemmParams): a k-step's 256 bytes of one
+  // 64-row group are contiguous, so wave w < 4 stages A's group m0 / 64 + w
+  // and wave w >= 4 B's group n0 / 64 + w - 4 with one 256-byte load beside
+  // the step's tiles (groups past the array read zeros: rows past M or N,
+  // whose data are zero). Stage layout: [2 k-step stages][A 1 KiB | B 1 KiB],
+  // tile group j at 256 j. Lane l's word of a group holds the bytes of its
+  // 4 row blocks (rows l & 15, + 16, + 32, + 48) at k-block l >> 4.
   uint8_t* sS = nullptr;
   if constexpr (MX) {
     __shared__ __attribute__((aligned(1024))) uint8_t s_mx[4096];
     sS = s_mx;
   }
-  const int KB = (K + 31) / 32;  // k-blocks holding data
   auto issue_scales = [&](int kt, int stage) {
     if constexpr (MX) {
       const bool is_b = wave >= 4;
-      const int row = (is_b ? n0 : m0) + 64 * (wave & 3) + lane;
+      const int groups = is_b ? p.mx_groups_b : p.mx_groups_a;
+      const int grp = (is_b ? n0 : m0) / 64 + (wave & 3);
       const v4i r = is_b ? make_rsrc(p.mx_b, p.mx_b_bytes) : make_rsrc(p.mx_a, p.mx_a_bytes);
       const uint32_t off =
-          row < (is_b ? N : M) ? (uint32_t)row * p.mx_ld + 4u * (uint32_t)kt : (uint32_t)r.z;
+          grp < groups ? ((uint32_t)(kt * groups + grp) * 64u + (uint32_t)lane) * 4u : (uint32_t)r.z;
       load_lds4(r, off, sS + stage * 2048 + (is_b ? 1024 : 0) + 256 * (wave & 3));
     }
   };
-  // This lane's byte (k-block lane >> 4 of step kt) for tile row / column
-  // rc of operand half (0 A, 1 B); padding blocks past K count as 1.
-  auto scale_byte = [&](int stage, int half, int rc, int kt) -> int {
-    const int g = lane >> 4;
-    const int v = sS[stage * 2048 + half * 1024 + 4 * rc + g];
-    return 4 * kt + g < KB ? v : 127;
+  // This lane's word of tile group j (0..3) of operand half (0 A, 1 B).
+  auto scale_word = [&](int stage, int half, int j) -> int {
+    return *(const int*)(sS + stage * 2048 + half * 1024 + 256 * j + 4 * lane);
   };
 
   v4f acc[MI][NI];  // NW = 8 (NW = 4: AccTile)
@@ -759,8 +757,10 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
   if constexpr (NW == 8) {
     v8i a[MI];   // A fragments of the step
     v8i bq[3];   // B fragments: in use and up to two groups ahead
-    int sa[MI] = {}, sb[NI] = {};  // MX: this lane's block-scale bytes of the step
-    const int r16 = lane & 15;
+    // MX: this lane's block-scale words of the step: A's for the wave's 64
+    // rows (byte mi), B's for its column groups 0 .. 3 and 4 .. 7 (byte ni & 3)
+    int sa = 0, sb[2] = {0, 0};
+    static_assert(!MX || (MI == 4 && NI == 8 && WTM == 64 && WTN == 128), "MX word layout");
 
     // One k-step. LOADS: issue the loads of step kt + 2 into this step's
     // stage after the barrier. NEXT: step kt + 1 exists (barrier, then its A
@@ -777,9 +777,11 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
       static_for<0, NI - 2>([&](auto I) {
         constexpr int ni = decltype(I)::value;
         bq[(ni + 2) % 3] = read_frag<B_KC, MX>(cB, wn + 16 * (ni + 2), lane);
-#pragma unroll
-        for (int mi = 0; mi < MI; ++mi)
-          acc[mi][ni] = mfma_s<FA, FB, MX>(bq[ni % 3], a[mi], acc[mi][ni], sb[ni], sa[mi]);
+        static_for<0, MI>([&](auto J) {
+          constexpr int mi = decltype(J)::value;
+          acc[mi][ni] =
+              mfma_s<FA, FB, MX, ni & 3, mi>(bq[ni % 3], a[mi], acc[mi][ni], sb[ni >> 2], sa);
+        });
 #pragma unroll
         for (int mi = 0; mi < MI; ++mi) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
@@ -796,44 +798,37 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
         __syncthreads();
         __builtin_amdgcn_sched_barrier(0);
         if (!LOADS && kt + 1 == KT_full && (krem & 15)) zero_tail(nA, nB);
-        // MX: B column groups 0 .. NI - 3 are done with their bytes
-        if constexpr (MX) {
-#pragma unroll
-          for (int ni = 0; ni < NI - 2; ++ni) sb[ni] = scale_byte(!odd, 1, wn + 16 * ni + r16, kt + 1);
-        }
+        // MX: B column groups 0 .. 3 are done with their word
+        if constexpr (MX) sb[0] = scale_word(!odd, 1, wn / 64);
       }
       // B column groups NI - 2 and NI - 1, taken row block by row block: once
       // both MFMAs of a[mi] have issued, a[mi] is refilled with the fragment
       // of step kt + 1; the loads of step kt + 2 go out two per row block.
-#pragma unroll
-      for (int mi = 0; mi < MI; ++mi) {
-        acc[mi][NI - 2] =
-            mfma_s<FA, FB, MX>(bq[(NI - 2) % 3], a[mi], acc[mi][NI - 2], sb[NI - 2], sa[mi]);
-        acc[mi][NI - 1] =
-            mfma_s<FA, FB, MX>(bq[(NI - 1) % 3], a[mi], acc[mi][NI - 1], sb[NI - 1], sa[mi]);
+      static_for<0, MI>([&](auto J) {
+        constexpr int mi = decltype(J)::value;
+        acc[mi][NI - 2] = mfma_s<FA, FB, MX, (NI - 2) & 3, mi>(bq[(NI - 2) % 3], a[mi],
+                                                                acc[mi][NI - 2], sb[1], sa);
+        acc[mi][NI - 1] = mfma_s<FA, FB, MX, (NI - 1) & 3, mi>(bq[(NI - 1) % 3], a[mi],
+                                                                acc[mi][NI - 1], sb[1], sa);
         if (LOADS) {
           issue_one(2 * mi, kt + 2, cA, cB);
           issue_one(2 * mi + 1, kt + 2, cA, cB);
           if (mi == MI - 1) issue_scales(kt + 2, odd);
         }
-        if (NEXT) {
-          a[mi] = read_frag<!A_MN, MX>(nA, wm + 16 * mi, lane);
-          if constexpr (MX) sa[mi] = scale_byte(!odd, 0, wm + 16 * mi + r16, kt + 1);
-        }
-      }
+        if (NEXT) a[mi] = read_frag<!A_MN, MX>(nA, wm + 16 * mi, lane);
+      });
       if (NEXT) {
         bq[0] = read_frag<B_KC, MX>(nB, wn, lane);
         bq[1] = read_frag<B_KC, MX>(nB, wn + 16, lane);
-        if constexpr (MX) {
-          sb[NI - 2] = scale_byte(!odd, 1, wn + 16 * (NI - 2) + r16, kt + 1);
-          sb[NI - 1] = scale_byte(!odd, 1, wn + 16 * (NI - 1) + r16, kt + 1);
+        if constexpr (MX) {  // every MFMA of this step has issued
+          sb[1] = scale_word(!odd, 1, wn / 64 + 1);
+          sa = scale_word(!odd, 0, wm / 64);
         }
       }
       static_for<0, MI>([&](auto I) {
         constexpr int i = decltype(I)::value;
-        // MX: the B bytes after the barrier, one A byte per row block, the
-        // last two B bytes at the end
-        constexpr int XS = MX ? 1 + (i == 0 ? NI - 2 : 0) + (i + 1 == MI ? 2 : 0) : 0;
+        // MX: one B word after the barrier, a B and the A word at the end
+        constexpr int XS = MX ? (i == 0 ? 1 : 0) + (i + 1 == MI ? 2 : 0) : 0;
         __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
         if (NEXT)
           __builtin_amdgcn_sched_group_barrier(0x100, (i + 1 < MI ? DSA : DSA + 2 * DSB) + XS, 0);
@@ -857,10 +852,9 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
       bq[0] = read_frag<B_KC, MX>(sB0, wn, lane);
       bq[1] = read_frag<B_KC, MX>(sB0, wn + 16, lane);
       if constexpr (MX) {
-#pragma unroll
-        for (int mi = 0; mi < MI; ++mi) sa[mi] = scale_byte(0, 0, wm + 16 * mi + r16, 0);
-#pragma unroll
-        for (int ni = 0; ni < NI; ++ni) sb[ni] = scale_byte(0, 1, wn + 16 * ni + r16, 0);
+        sa = scale_word(0, 0, wm / 64);
+        sb[0] = scale_word(0, 1, wn / 64);
+        sb[1] = scale_word(0, 1, wn / 64 + 1);
       }
     }
     int kt = 0;

@@ -54,13 +54,19 @@ struct GemmParams {
   // accumulator with the power-of-two product of the epilogue; NULL = 1.
   const float* ch_a;
   const float* ch_b;
-  // MX block scales (MX kernels only): E8M0 bytes [M][mx_ld] for A and
-  // [N][mx_ld] for B, byte k / 32 of a row scaling that row's k; mx_ld =
-  // 4 * ceil(K / 128); byte sizes of the arrays for the buffer range checks.
+  // MX block scales (MX kernels only), packed by launch_mx_pack: per 128-k
+  // step and 64-row group (mx_groups_* = ceil(rows / 64) groups), 64 words,
+  // word 16 g + r holding the bytes of rows r, r + 16, r + 32, r + 48 of the
+  // group at k-block g of the step; byte sizes for the buffer range checks.
   const uint8_t* mx_a;
   const uint8_t* mx_b;
-  uint32_t mx_ld, mx_a_bytes, mx_b_bytes;
+  int mx_groups_a, mx_groups_b;
+  uint32_t mx_a_bytes, mx_b_bytes;
 };
+
+// Packed MX block scales (see GemmParams) from row-major bytes src[r * ld + b].
+hipError_t launch_mx_pack(const uint8_t* src, int rows, int K, int ld, uint8_t* dst,
+                          hipStream_t s);
 
 // fuse: launch the kernels with the fused residual add / activation / pre_out
 // epilogue (the plain kernels otherwise).

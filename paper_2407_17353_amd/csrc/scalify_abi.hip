@@ -136,7 +136,24 @@ size_t layernorm_bwd_ws(int64_t R, int64_t D) {
 
 extern "C" {
 
-int64_t scalify_mx_block_scale_ld(int64_t K) { return K < 1 ? 0 : 4 * ((K + 127) / 128); }
+int64_t scalify_mx_packed_bytes(int64_t rows, int64_t K) {
+  if (rows < 1 || K < 1) return 0;
+  return 256 * ((K + 127) / 128) * ((rows + 63) / 64);
+}
+
+scalify_status scalify_mx_pack_block_scales(const uint8_t* src, int64_t rows, int64_t K,
+                                            int64_t src_ld, uint8_t* dst, void* stream) {
+  if (rows < 0 || K < 0 || rows > kMaxDim || K > kMaxDim) return SCALIFY_ERR_SHAPE;
+  if (rows == 0 || K == 0) return SCALIFY_OK;
+  if (!src || !dst) return SCALIFY_ERR_NULL;
+  if (src_ld < (K + 31) / 32 || scalify_mx_packed_bytes(rows, K) >= ((int64_t)1 << 32) ||
+      rows * src_ld >= ((int64_t)1 << 32))
+    return SCALIFY_ERR_SHAPE;
+  if ((uintptr_t)dst & 3u) return SCALIFY_ERR_ALIGN;
+  return launch_mx_pack(src, (int)rows, (int)K, (int)src_ld, dst, (hipStream_t)stream) == hipSuccess
+             ? SCALIFY_OK
+             : SCALIFY_ERR_HIP;
+}
 
 int32_t scalify_matmul_scale_log2(int64_t K) {
   // Largest e with 2^e <= sqrt(K), i.e. 4^e <= K (integer arithmetic only).
@@ -199,7 +216,7 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
     return SCALIFY_ERR_ALIGN;
   const bool fused = is_fused(opts);
   const bool mx = has_mx(opts);
-  const int64_t mx_ld = scalify_mx_block_scale_ld(K);
+  const int64_t mx_a_bytes = scalify_mx_packed_bytes(M, K), mx_b_bytes = scalify_mx_packed_bytes(N, K);
   if (mx) {
     // an array of no bytes (M, N or K zero) may be NULL
     if ((!opts->a_block_scale && M * K > 0) || (!opts->b_block_scale && N * K > 0))
@@ -207,7 +224,7 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
     if (fused) return SCALIFY_ERR_VALUE;
     if (((uintptr_t)opts->a_block_scale | (uintptr_t)opts->b_block_scale) & 3u)
       return SCALIFY_ERR_ALIGN;
-    if (M * mx_ld >= ((int64_t)1 << 32) || N * mx_ld >= ((int64_t)1 << 32)) return SCALIFY_ERR_SHAPE;
+    if (mx_a_bytes >= ((int64_t)1 << 32) || mx_b_bytes >= ((int64_t)1 << 32)) return SCALIFY_ERR_SHAPE;
   }
   // 32-bit byte offsets inside the GEMM kernel, including the range-checked
   // reads of up to one tile past the last stored row.
@@ -278,9 +295,10 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
   // (the block-scale kernels run whenever the product has terms: K > 0)
   p.mx_a = mx && K > 0 ? opts->a_block_scale : nullptr;
   p.mx_b = mx && K > 0 ? opts->b_block_scale : nullptr;
-  p.mx_ld = (uint32_t)mx_ld;
-  p.mx_a_bytes = (uint32_t)(M * mx_ld);
-  p.mx_b_bytes = (uint32_t)(N * mx_ld);
+  p.mx_groups_a = (int)((M + 63) / 64);
+  p.mx_groups_b = (int)((N + 63) / 64);
+  p.mx_a_bytes = (uint32_t)mx_a_bytes;
+  p.mx_b_bytes = (uint32_t)mx_b_bytes;
   hipEvent_t* ev = (hipEvent_t*)opts->events;
   if (ev && ev[0] && hipEventRecord(ev[0], s) != hipSuccess) return SCALIFY_ERR_HIP;
   if (M > 0 && N > 0) {

@@ -59,7 +59,7 @@ def int_grid(shape, fmt: int, seed: int, device="cpu", vmax: int = 8):
 
 
 def mx_block_scales(rows: int, K: int, seed: int, lo: int = -8, hi: int = 8, device="cpu"):
-    """E8M0 block-scale bytes [rows][4 * ceil(K / 128)] (one per 32 k,
+    """Row-major E8M0 block-scale bytes [rows][4 * ceil(K / 128)] (one per 32 k,
     padded to whole 128-k steps): 127 + an exponent uniform in [lo, hi], the
     spread of per-block scales of FP8 data quantized block by block."""
     ld = 4 * ((K + 127) // 128)

@@ -201,14 +201,19 @@ def test_fused_workspace_sizes():
     assert sc.load_library().scalify_matmul_workspace_size_opts(10, 10, None) == 0
 
 
-def test_mx_block_scale_row_length():
-    """One byte per 32 k, padded to whole 128-k steps; the oracle's helper
-    states the same layout independently."""
-    from oracle import oracle as orc
-    for K in (1, 31, 32, 33, 127, 128, 129, 200, 8192, 11008):
-        assert sc.scalify_mx_block_scale_ld(K) == 4 * ((K + 127) // 128) == orc.mx_block_scale_ld(K)
-        assert sc.scalify_mx_block_scale_ld(K) >= (K + 31) // 32
-    assert sc.scalify_mx_block_scale_ld(0) == 0
+def test_mx_packed_bytes_and_pack_argument_errors():
+    """256 bytes per 128-k step and 64-row group; the pack entry point checks
+    its arguments before launching anything."""
+    for rows, K in ((1, 1), (64, 128), (65, 129), (8192, 8192), (11008, 4096)):
+        assert sc.scalify_mx_packed_bytes(rows, K) == 256 * ((K + 127) // 128) * ((rows + 63) // 64)
+    assert sc.scalify_mx_packed_bytes(0, 64) == 0 and sc.scalify_mx_packed_bytes(64, 0) == 0
+    lib = sc.load_library()
+    pack = lib.scalify_mx_pack_block_scales
+    assert pack(None, 0, 64, 2, None, None) == 0           # nothing to pack, nothing launched
+    assert pack(None, 16, 64, 2, FAKE, None) == 1           # NULL src
+    assert pack(FAKE, 16, 64, 1, FAKE + 4096, None) == 3    # src_ld < ceil(K / 32)
+    assert pack(FAKE, -1, 64, 2, FAKE + 4096, None) == 3    # negative rows
+    assert pack(FAKE, 16, 64, 2, FAKE + 4098, None) == 5    # dst not 4-byte aligned
 
 
 def fused_opts(residual=None, act=sc.ACT_NONE, pre_out=None, out_dtype=sc.E4M3,

@@ -45,10 +45,11 @@ def _mx_run(A_st, fa, ta, sa, B_st, fb, tb, sb, fout, PA, PB, mode=sc.RESCALE_AM
     acc = torch.empty((M, N), dtype=torch.float32, device=DEV) if want_acc else None
     stat_in = torch.tensor([amax_in], dtype=torch.float32, device=DEV)
     stat_out = torch.empty(1, dtype=torch.float32, device=DEV)
+    pa = None if PA is None else sc.scalify_mx_pack_block_scales(PA.to(DEV), K)
+    pb = None if PB is None else sc.scalify_mx_pack_block_scales(PB.to(DEV), K)
     sc.scalify_matmul(a, b, out, rescale=mode, saturate=sat, acc_out=acc, amax_out=stat_out,
                       amax_in=stat_in if mode == sc.RESCALE_DELAYED else None,
-                      a_block_scale=None if PA is None else PA.to(DEV),
-                      b_block_scale=None if PB is None else PB.to(DEV))
+                      a_block_scale=pa, b_block_scale=pb)
     torch.cuda.synchronize()
     codes = out.data.cpu().numpy()
     if fout == sc.F16:
@@ -190,6 +191,23 @@ def test_padding_bytes_are_not_used():
     assert np.array_equal(r0[3].view(np.uint32), r1[3].view(np.uint32))
     assert np.array_equal(r0[0], r1[0]) and r0[1:3] == r1[1:3]
     _check(r1, A, sc.E4M3, False, 0, B, sc.E4M3, False, 0, sc.E5M2, PA2, PB2, sc.RESCALE_AMAX)
+
+
+@pytest.mark.parametrize("rows,K", [(1, 1), (17, 65), (64, 128), (300, 1000), (130, 4096 + 32)])
+def test_pack_order(rows, K):
+    """The packed order written out independently with numpy: word
+    ((t * G + q) * 64 + 16 g + r) holds rows 64 q + r + 16 i (byte i) at
+    k-block 4 t + g, with 127 outside the array."""
+    say(f"case mx pack {rows}x{K}")
+    src = wl.mx_block_scales(rows, K, 961)
+    got = sc.scalify_mx_pack_block_scales(src.to(DEV), K).cpu().numpy()
+    nb, T, G = (K + 31) // 32, (K + 127) // 128, (rows + 63) // 64
+    full = np.full((G * 64, 4 * T), 127, np.uint8)
+    full[:rows, :nb] = src.numpy()[:, :nb]
+    want = full.reshape(G, 4, 16, T, 4)            # [q][i][r][t][g]
+    want = want.transpose(3, 0, 4, 2, 1).reshape(-1)  # [t][q][g][r][i]
+    assert got.size == sc.scalify_mx_packed_bytes(rows, K) == want.size
+    assert np.array_equal(got, want)
 
 
 def test_empty_and_zero_depth():
