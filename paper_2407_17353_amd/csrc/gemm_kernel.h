@@ -269,19 +269,20 @@ __device__ __forceinline__ v4f mfma_s(const v8i& bfrag, const v8i& afrag, const 
 // One LDS read S of a fragment (read_frag split into its instructions, so
 // that they can be interleaved one by one with MFMAs): KC parts 0, 1 are
 // the two 16-byte halves, MC parts 0 .. 3 the four transposing reads.
-template <bool KC, int S>
+template <bool KC, int S, bool HWK = false>
 __device__ __forceinline__ void read_frag_part(v8i& f, const uint8_t* lds, int base, int lane) {
   if constexpr (KC) {
     const int r = base + (lane & 15);
     const int g = lane >> 4;
-    const v4i h = *(const v4i*)(lds + r * 128 + (((2 * g + S) ^ swz_kc(r)) * 16));
+    const int c = HWK ? 4 * S + g : 2 * g + S;  // 16-byte k chunk (read_frag's order)
+    const v4i h = *(const v4i*)(lds + r * 128 + ((c ^ swz_kc(r)) * 16));
     f[4 * S + 0] = h.x;
     f[4 * S + 1] = h.y;
     f[4 * S + 2] = h.z;
     f[4 * S + 3] = h.w;
   } else {
     const int t = lane & 15, g = lane >> 4;
-    const int k = 32 * g + 8 * S + (t >> 1);
+    const int k = (HWK ? 64 * (S >> 1) + 16 * g + 8 * (S & 1) : 32 * g + 8 * S) + (t >> 1);
     const int off = k * 256 + (((base >> 4) ^ swz_mc(k)) * 16) + (t & 1) * 8;
     const v2i v = __builtin_amdgcn_ds_read_tr8_b64_v2i32((LDS_AS v2i*)(lds + off));
     f[2 * S] = v.x;
@@ -371,6 +372,15 @@ struct AccTile;
 #define SCALIFY_ACC_TILE(t, r, r0, r1, r2, r3)                                                  \
   template <>                                                                                  \
   struct AccTile<t> {                                                                          \
+    /* MX block scales: byte OB of sb (B fragment) and OA of sa (A fragment) */                \
+    template <int FA, int FB, int OB, int OA>                                                  \
+    static __device__ __forceinline__ void mfma_mx(const v8i& b, const v8i& a, int sb, int sa) { \
+      asm volatile("v_mfma_scale_f32_16x16x128_f8f6f4 a[" r "], %0, %1, a[" r "], %2, %3 "     \
+                   "op_sel:[%4,%5,0] op_sel_hi:[%6,%7,0] cbsz:%8 blgp:%9"                     \
+                   :: "v"(b), "v"(a), "v"(sb), "v"(sa), "n"(OB & 1), "n"(OA & 1), "n"(OB >> 1), \
+                      "n"(OA >> 1), "n"(FB), "n"(FA)                                           \
+                   : "a" r0, "a" r1, "a" r2, "a" r3);                                          \
+    }                                                                                          \
     template <int FA, int FB>                                                                  \
     static __device__ __forceinline__ void mfma(const v8i& b, const v8i& a) {                  \
       if constexpr (FB == 0 && FA == 0)                                                        \
@@ -649,8 +659,8 @@ template <bool A_MN, bool B_KC, int FA, int FB, int EPI, bool FUSE, int NW, bool
 __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
   static_assert(NW == 8 || (NW == 4 && !FUSE), "the fused epilogue runs on the 8-wave kernel");
   static_assert(FUSE || !CH, "channel scales are part of the fused epilogue");
-  static_assert(!MX || (NW == 8 && !FUSE && EPI != EPI_INTER16),
-                "block scales: 8-wave kernel, plain epilogue, fp32 intermediate or direct cast");
+  static_assert(!MX || (!FUSE && (EPI == EPI_INTER32 || (EPI == EPI_DIRECT && NW == 8))),
+                "block scales: plain epilogue, fp32 intermediate or direct cast (8 waves)");
   using C = WaveCfg<NW>;
   constexpr int WAVES = C::WAVES, WAVES_N = C::WAVES_N, WTM = C::WTM, WTN = C::WTN;
   constexpr int MI = C::MI, NI = C::NI, BPW = C::BPW, LOADS_PER_STEP = C::LOADS_PER_STEP;
@@ -719,6 +729,17 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
     __shared__ __attribute__((aligned(1024))) uint8_t s_mx[4096];
     sS = s_mx;
   }
+  // 4 waves: wave w stages group w of A (half 0) and of B (half 1), one call each.
+  auto issue_scale_half = [&](int kt, int stage, bool is_b) {
+    if constexpr (MX) {
+      const int groups = is_b ? p.mx_groups_b : p.mx_groups_a;
+      const int grp = (is_b ? n0 : m0) / 64 + wave;
+      const v4i r = is_b ? make_rsrc(p.mx_b, p.mx_b_bytes) : make_rsrc(p.mx_a, p.mx_a_bytes);
+      const uint32_t off =
+          grp < groups ? ((uint32_t)(kt * groups + grp) * 64u + (uint32_t)lane) * 4u : (uint32_t)r.z;
+      load_lds4(r, off, sS + stage * 2048 + (is_b ? 1024 : 0) + 256 * wave);
+    }
+  };
   auto issue_scales = [&](int kt, int stage) {
     if constexpr (MX) {
       const bool is_b = wave >= 4;
@@ -895,6 +916,9 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
     constexpr int RX = MI < (NI - 2) * DSB ? MI : (NI - 2) * DSB;  // B reads issued before X
     v8i af[2][MI];
     v8i bf[NI];
+    // MX: block-scale words by step parity, like af: A's for the wave's
+    // rows 0 .. 63 and 64 .. 127 (byte mi & 3), B's for its columns likewise
+    int sa[2][2] = {}, sb[2][2] = {};
 
     auto head = [&](auto par_tag, int kt) {
       constexpr int P = decltype(par_tag)::value;
@@ -904,10 +928,14 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
       static_for<0, H * MI>([&](auto I) {
         constexpr int i = decltype(I)::value;
         constexpr int ni = i / MI, mi = i % MI;
-        AccTile<mi * NI + ni>::template mfma<FA, FB>(bf[ni], af[P][mi]);
+        if constexpr (MX)
+          AccTile<mi * NI + ni>::template mfma_mx<FA, FB, ni & 3, mi & 3>(
+              bf[ni], af[P][mi], sb[P][ni >> 2], sa[P][mi >> 2]);
+        else
+          AccTile<mi * NI + ni>::template mfma<FA, FB>(bf[ni], af[P][mi]);
         if constexpr (i < (NI - 2) * DSB) {
           constexpr int g = 2 + i / DSB;  // column group whose fragment part is read
-          read_frag_part<B_KC, i % DSB>(bf[g], cB, wn + 16 * g, lane);
+          read_frag_part<B_KC, i % DSB, MX>(bf[g], cB, wn + 16 * g, lane);
         }
         if constexpr (i == MI - 1) {
           // X: this wave's reads of step kt's A fragments (issued before
@@ -921,12 +949,15 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
           static_for<j * BPW / AS, (j + 1) * BPW / AS>([&](auto J) {
             issue_one(decltype(J)::value, kt + 2, cA, cB);
           });
+          // MX: the A scale words of step kt + 2 after its A tile loads
+          if constexpr (i + 1 == H * MI) issue_scale_half(kt + 2, odd, false);
         }
       });
       // Y: step kt + 1 has landed (its A loads went out in the previous
-      // head, its B loads in the previous tail; only this head's BPW loads
-      // may be outstanding) and this wave's B reads of step kt are done.
-      wait_vmcnt<BPW>();
+      // head, its B loads in the previous tail; only this head's BPW loads,
+      // and with MX its A scale load, may be outstanding) and this wave's B
+      // reads of step kt are done.
+      wait_vmcnt<BPW + (MX ? 1 : 0)>();
       wait_lgkmcnt<0>();
       __builtin_amdgcn_s_barrier();
       if (kt + 1 == KT_full && (krem & 15)) zero_tail(odd ? sA0 : sA1, odd ? sB0 : sB1);
@@ -941,34 +972,56 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
       static_for<0, TS>([&](auto I) {
         constexpr int i = decltype(I)::value;
         constexpr int mi = i / (NI - H), ni = H + i % (NI - H);
-        AccTile<mi * NI + ni>::template mfma<FA, FB>(bf[ni], af[P][mi]);
+        if constexpr (MX)
+          AccTile<mi * NI + ni>::template mfma_mx<FA, FB, ni & 3, mi & 3>(
+              bf[ni], af[P][mi], sb[P][ni >> 2], sa[P][mi >> 2]);
+        else
+          AccTile<mi * NI + ni>::template mfma<FA, FB>(bf[ni], af[P][mi]);
         // B loads [i * BPW / TS, (i + 1) * BPW / TS) of step kt + 2
         static_for<i * BPW / TS, (i + 1) * BPW / TS>([&](auto J) {
           issue_one(BPW + decltype(J)::value, kt + 2, cA, cB);
         });
+        // MX: the B scale words of step kt + 2 after its B tile loads
+        if constexpr (i + 1 == TS) issue_scale_half(kt + 2, odd, true);
         // reads [i * BP / TS, (i + 1) * BP / TS) of the next step's B fragments 0, 1
         static_for<i * BP / TS, (i + 1) * BP / TS>([&](auto Q) {
           constexpr int q = decltype(Q)::value;
-          read_frag_part<B_KC, q % DSB>(bf[q / DSB], nB, wn + 16 * (q / DSB), lane);
+          read_frag_part<B_KC, q % DSB, MX>(bf[q / DSB], nB, wn + 16 * (q / DSB), lane);
         });
         // A reads [i * AR / TS, (i + 1) * AR / TS) of the next step, into the other buffer
         static_for<i * (MI * DSA) / TS, (i + 1) * (MI * DSA) / TS>([&](auto Q) {
           constexpr int q = decltype(Q)::value;
-          read_frag_part<!A_MN, q % DSA>(af[P ^ 1][q / DSA], nA, wm + 16 * (q / DSA), lane);
+          read_frag_part<!A_MN, q % DSA, MX>(af[P ^ 1][q / DSA], nA, wm + 16 * (q / DSA), lane);
         });
       });
+      if constexpr (MX) {  // the next step's scale words, into the other buffer
+        sa[P ^ 1][0] = scale_word(!odd, 0, wm / 64);
+        sa[P ^ 1][1] = scale_word(!odd, 0, wm / 64 + 1);
+        sb[P ^ 1][0] = scale_word(!odd, 1, wn / 64);
+        sb[P ^ 1][1] = scale_word(!odd, 1, wn / 64 + 1);
+      }
     };
 
     if (KT > 0) {
       issue_all(0, sA0, sB0);
+      issue_scale_half(0, 0, false);
+      issue_scale_half(0, 0, true);
       issue_all(1, sA1, sB1);
-      wait_vmcnt<LOADS_PER_STEP>();
+      issue_scale_half(1, 1, false);
+      issue_scale_half(1, 1, true);
+      wait_vmcnt<LOADS_PER_STEP + (MX ? 2 : 0)>();
       __syncthreads();
       if (KT_full == 0 && (krem & 15)) zero_tail(sA0, sB0);
 #pragma unroll
       for (int mi = 0; mi < MI; ++mi) af[0][mi] = read_frag<!A_MN, MX>(sA0, wm + 16 * mi, lane);
       bf[0] = read_frag<B_KC, MX>(sB0, wn, lane);
       bf[1] = read_frag<B_KC, MX>(sB0, wn + 16, lane);
+      if constexpr (MX) {
+        sa[0][0] = scale_word(0, 0, wm / 64);
+        sa[0][1] = scale_word(0, 0, wm / 64 + 1);
+        sb[0][0] = scale_word(0, 1, wn / 64);
+        sb[0][1] = scale_word(0, 1, wn / 64 + 1);
+      }
       using P0 = std::integral_constant<int, 0>;
       using P1 = std::integral_constant<int, 1>;
       head(P0{}, 0);
@@ -1211,21 +1264,28 @@ hipError_t launch_fmt(const GemmParams& p, int epi, hipStream_t s) {
   }
 }
 
-// MX block scales: the 8-wave kernel with the fp32 intermediate (NONE,
-// AMAX) or the direct cast (DELAYED); one source file per layout
-// (gemm_<layout>_mx.hip).
+// MX block scales: the 4-wave kernel with the fp32 intermediate (NONE,
+// AMAX), the 8-wave kernel with the direct cast (DELAYED) and for A and B
+// both stored k-major (A [K][M], B [K][N]), whose 4-wave variant does not
+// fit its registers (the build check rejects its spills); one source file
+// per layout (gemm_<layout>_mx.hip).
+constexpr int mx_waves(bool a_mn, bool b_kc, int epi) {
+  return (epi == EPI_DIRECT || (a_mn && !b_kc)) ? 8 : 4;
+}
 template <bool A_MN, bool B_KC>
 hipError_t launch_layout_mx(const GemmParams& p, int fa, int fb, int epi, hipStream_t s);
 
 template <bool A_MN, bool B_KC, int FA, int FB>
 hipError_t launch_mx(const GemmParams& p, int epi, hipStream_t s) {
-  const dim3 grid(p.tiles_m * p.tiles_n), block(WaveCfg<8>::NTHR);
+  const dim3 grid(p.tiles_m * p.tiles_n);
   if (epi == EPI_DIRECT)
     hipLaunchKernelGGL((gemm_kernel<A_MN, B_KC, FA, FB, EPI_DIRECT, false, 8, false, true>), grid,
-                       block, 0, s, p);
+                       dim3(WaveCfg<8>::NTHR), 0, s, p);
   else
-    hipLaunchKernelGGL((gemm_kernel<A_MN, B_KC, FA, FB, EPI_INTER32, false, 8, false, true>), grid,
-                       block, 0, s, p);
+    hipLaunchKernelGGL(
+        (gemm_kernel<A_MN, B_KC, FA, FB, EPI_INTER32, false, mx_waves(A_MN, B_KC, EPI_INTER32), false,
+                     true>),
+        grid, dim3(WaveCfg<mx_waves(A_MN, B_KC, EPI_INTER32)>::NTHR), 0, s, p);
   return hipGetLastError();
 }
 
