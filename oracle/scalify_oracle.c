@@ -459,13 +459,25 @@ static int32_t finish(const float* v, int64_t n, int32_t e_in, int mode, int32_t
     return e_out;
 }
 
+int32_t or_finish_pre(const float* w, int64_t n, int32_t e_w, int32_t e_cc, int mode, int32_t t,
+                      float stat_in, int sat, int out_fmt, void* out, float* amax_out);
+
 /* Epilogue of the scaled matmul (Section 3.2 propagation + Section 3.3
  * dynamic rescale + stage-2 cast of Section 2), applied to an fp32
  * accumulator acc[n] (n = M*N).
- *   e_c  = matmul scale rule for K; data = acc * 2^-e_c is exact.
- *   value of data = data * 2^(e_a + e_b + e_c).
+ *   e_c  = matmul scale rule for K; the propagated data is acc * 2^-e_c, a
+ *   power-of-two division of the accumulator, with value
+ *   data * 2^(e_a + e_b + e_c).
+ * That data is never rounded to fp32 on its own: where acc * 2^-e_c would
+ * be an fp32 subnormal, rounding it first and then shifting it again by the
+ * rescale would round twice. The statistic is therefore taken on acc, with
+ * e_c subtracted from its exponent (floor(log2(amax * 2^-e_c)) =
+ * floor(log2 amax) - e_c exactly), and each code is the cast of acc after
+ * one power-of-two shift to the output scale: or_finish_pre with the
+ * pre-cast value w = acc, e_w = e_a + e_b and the statistic offset e_c.
  * Returns 0 on success, -1 on a non-power-of-two input scale.
- * Outputs: codes, *e_out (output scale = 2^e_out), *amax (of acc*2^-e_c). */
+ * Outputs: codes, *e_out (output scale = 2^e_out), *amax (of acc*2^-e_c,
+ * rounded once to fp32). */
 static int matmul_epilogue_impl(const float* acc, int64_t n, float s_a, float s_b, int64_t K,
                                 int mode, int32_t t, int sat, int out_fmt,
                                 void* out, int32_t* e_out, float* amax, float stat_in)
@@ -474,15 +486,8 @@ static int matmul_epilogue_impl(const float* acc, int64_t n, float s_a, float s_
     int32_t e_a = or_scale_exponent(s_a, &ok_a);
     int32_t e_b = or_scale_exponent(s_b, &ok_b);
     int32_t e_c = or_matmul_scale_log2(K);
-    float* data;
-    int64_t i;
     if (!ok_a || !ok_b) return -1;
-    data = (float*)malloc(sizeof(float) * (size_t)(n > 0 ? n : 1));
-    for (i = 0; i < n; ++i) data[i] = ldexpf(acc[i], -e_c);
-    /* The propagated data carries 2^(e_a+e_b+e_c). finish() shifts acc-based
-     * data by e_in - e_out, which equals -(e_r) plus any clamp correction. */
-    *e_out = finish(data, n, e_a + e_b + e_c, mode, t, sat, out_fmt, out, amax, stat_in);
-    free(data);
+    *e_out = or_finish_pre(acc, n, e_a + e_b, e_c, mode, t, stat_in, sat, out_fmt, out, amax);
     return 0;
 }
 

@@ -427,6 +427,52 @@ def test_hand_derived_examples():
         assert e_out == case["out_scale_log2"], case["name"]
 
 
+def _pair(v):
+    """[mantissa, exponent] of the epilogue goldens -> exact fp32."""
+    return math.ldexp(float(v[0]), int(v[1]))
+
+
+def test_epilogue_hand_examples_subnormal_accumulators():
+    """Hand-derived epilogues of fp32-subnormal accumulators
+    (tests/golden/epilogue_examples.json): the propagated data acc * 2^-e_c
+    (Section 3.2) is an exact division, not an fp32 value of its own, so the
+    statistic and every code come from acc through one power-of-two shift
+    (Section 3.3 rebalance); rounding the data first changes scale and codes."""
+    with open(os.path.join(GOLDEN, "epilogue_examples.json")) as f:
+        cases = json.load(f)["cases"]
+    fmt_of = {"e4m3": orc.E4M3, "e5m2": orc.E5M2, "f16": orc.F16}
+    for c in cases:
+        acc = np.array([[_pair(v) for v in row] for row in c["acc"]], dtype=np.float32)
+        # the accumulators are what the derivation says: fp32 subnormals, exact
+        assert np.all(np.abs(acc) < np.float32(2.0 ** -126)) and np.all(acc != 0), c["name"]
+        codes, e_out, amax = orc.matmul_epilogue(
+            acc, 2.0 ** c["a_scale_log2"], 2.0 ** c["b_scale_log2"], c["K"],
+            orc.RESCALE_AMAX if c["mode"] == "amax" else orc.RESCALE_NONE, 0, True,
+            fmt_of[c["out_fmt"]])
+        assert codes.tolist() == c["out_codes"], (c["name"], codes.tolist())
+        assert e_out == c["out_scale_log2"], (c["name"], e_out)
+        assert amax == _pair(c["amax"]), (c["name"], amax)
+
+
+def test_epilogue_is_one_rounding_of_the_exact_product_value():
+    """Model invariance (Section 1: scaling leaves the computation unchanged)
+    down to the fp32 subnormal range: each decoded output code times the
+    output scale is the nearest E4M3 value (in output-scale units) of the
+    exact value acc * s_a * s_b, whatever e_c the depth K gives."""
+    rng = np.random.default_rng(23)
+    units = rng.integers(-2 ** 20, 2 ** 20, 400)
+    acc = np.ldexp(units.astype(np.float64), -149 - rng.integers(0, 4, 400)).astype(np.float32)
+    for K in (1, 4, 64, 4096):
+        codes, e_out, _ = orc.matmul_epilogue(acc, 2.0 ** 70, 2.0 ** 50, K)
+        exact = acc.astype(np.float64) * 2.0 ** 120
+        want = orc.cast(orc.E4M3, np.ldexp(exact, -e_out).astype(np.float32))
+        # the shifted exact values are fp32 numbers (a power-of-two shift of
+        # an fp32 value that stays normal), so casting them is one rounding
+        assert np.array_equal(np.ldexp(np.ldexp(exact, -e_out).astype(np.float32).astype(np.float64),
+                                       e_out), exact)
+        assert np.array_equal(codes, want), K
+
+
 def test_nan_sign_is_kept_through_decode_and_cast():
     """Reading R7: a NaN keeps its sign bit (as torch's float8 casts do)."""
     codes = np.array([0x7F, 0xFF], np.uint8)

@@ -9,6 +9,9 @@ to the inputs, the reduction to the unscaled accumulator (all bytes 127)
 and to per-channel factors (constant bytes along k), the decomposition of
 the sum into its 32-k blocks, and the invariance under storage order.
 """
+import json
+import math
+import os
 from fractions import Fraction
 
 import numpy as np
@@ -150,3 +153,23 @@ def test_storage_order_and_sampled_positions_agree():
     absA, absB = A & 0x7F, B & 0x7F  # sign-magnitude codes: |value|
     l1_ref = orc.matmul_acc_mx(absA, orc.E5M2, False, absB, orc.E4M3, False, sa, sb)
     assert np.allclose(l1, l1_ref[ii, jj], rtol=1e-6)
+
+
+def test_mx_golden_subnormal_accumulator():
+    """Hand-derived (tests/golden/epilogue_examples.json): block scales can
+    make the accumulator an fp32 subnormal; the block-scaled sum keeps it
+    exactly and the epilogue casts it with one power-of-two shift."""
+    path = os.path.join(os.path.dirname(__file__), "golden", "epilogue_examples.json")
+    with open(path) as f:
+        cases = json.load(f)["mx_cases"]
+    for c in cases:
+        A = np.array(c["a_codes"], dtype=np.uint8)
+        B = np.array(c["b_codes"], dtype=np.uint8)
+        K = A.shape[1]
+        acc = orc.matmul_acc_mx(A, orc.E4M3, False, B, orc.E4M3, False,
+                                np.array(c["a_block"], np.uint8), np.array(c["b_block"], np.uint8))
+        want = [[math.ldexp(v[0], v[1]) for v in row] for row in c["acc"]]
+        assert acc.tolist() == want, c["name"]
+        codes, e_out, _ = orc.matmul_epilogue(acc, 2.0 ** c["a_scale_log2"],
+                                              2.0 ** c["b_scale_log2"], K, orc.RESCALE_AMAX)
+        assert codes.tolist() == c["out_codes"] and e_out == c["out_scale_log2"], c["name"]
