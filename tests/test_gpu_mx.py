@@ -21,7 +21,7 @@ import torch
 from oracle import oracle as orc
 from paper_2407_17353_amd import binding as sc
 from paper_2407_17353_amd import workloads as wl
-from tests.helpers import _compare_acc, check_p1, say, stored_with_padding
+from tests.helpers import FMT, _compare_acc, check_p1, record, say, stored_with_padding
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -241,3 +241,33 @@ def test_headline_shape_sampled():
                                    PB.numpy(), ii, jj)
     _compare_acc(acc[ii, jj], ref, l1, case.K)
     check_p1(codes, e_out, amax, acc, case.K, case.a_scale_log2, case.b_scale_log2, case.fout)
+
+
+@pytest.mark.parametrize("fout", [sc.E4M3, sc.E5M2])
+def test_subnormal_accumulators_single_shift(fout):
+    """Block factors of 2^-140 make every product, and so the accumulators,
+    fp32 subnormals: P1 checks that the statistic and every code come from
+    the GPU's accumulator through one power-of-two shift (reading R30), the
+    case the plain FP8 path never reaches (its accumulators are >= 2^-32)."""
+    M, N, K = 64, 80, 256
+    say(f"case mx subnormal accumulators fout={fout}")
+    A = _codes((M, K), sc.E4M3, 921)
+    B = _codes((K, N), sc.E4M3, 922)
+    ld = orc.mx_block_scale_ld(K)
+    PA = torch.full((M, ld), 127 - 70, dtype=torch.uint8)
+    PB = torch.full((N, ld), 127 - 70, dtype=torch.uint8)
+    codes, e_out, amax, acc = _mx_run(A, 0, False, 60, B, 0, False, 60, fout, PA, PB)
+    nz = acc[acc != 0]
+    record("mx_subnormal", fout=FMT[fout], nonzero=int(nz.size),
+           subnormal=int(np.count_nonzero(np.abs(nz) < 2.0 ** -126)), e_out=e_out)
+    say(f"  nonzero acc {nz.size}, subnormal {np.count_nonzero(np.abs(nz) < 2.0 ** -126)}")
+    assert nz.size > 0 and np.all(np.abs(nz) < 2.0 ** -126)
+    check_p1(codes, e_out, amax, acc, K, 60, 60, fout)
+    # P2 against the oracle's block-scaled sum (exact in fp64, one rounding)
+    ref = orc.matmul_acc_mx(A.numpy(), 0, False, B.numpy(), 0, False, PA.numpy(), PB.numpy())
+    l1 = orc.matmul_acc_mx(A.numpy() & 0x7F, 0, False, B.numpy() & 0x7F, 0, False,
+                           PA.numpy(), PB.numpy())
+    err = np.abs(acc.astype(np.float64) - ref.astype(np.float64))
+    record("mx_subnormal_p2", fout=FMT[fout], max_err=float(err.max()),
+           max_l1=float(l1.max()), exact=int(np.count_nonzero(err == 0)), n=int(err.size))
+    say(f"  P2 max |acc - ref| {err.max():.3g} (l1 max {l1.max():.3g}), exact {np.count_nonzero(err == 0)}")
