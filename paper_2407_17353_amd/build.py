@@ -7,9 +7,11 @@ for all device code.
 The one-wave-per-SIMD GEMM kernels keep their accumulators in AGPRs that only
 their inline asm names (AccTile in csrc/gemm_kernel.h); the compiler does not
 know these registers hold values. The build therefore disassembles the GEMM
-objects and fails if, in any kernel that uses those accumulators, the
-compiler placed values of its own in AGPRs (an AGPR written from a VGPR or
-moved, which is how it spills) or used scratch memory.
+objects and fails if, in any kernel that uses those accumulators, any
+instruction other than the accumulator asm's own forms (an MFMA whose
+destination and C operand are the same a[n:n+3], a write of 0, a read into a
+VGPR) names an AGPR -- the compiler spilling into AGPRs or using one as the
+data of a load or an MFMA operand -- or the kernel uses scratch memory.
 """
 from __future__ import annotations
 
@@ -45,7 +47,23 @@ def _llvm(tool: str) -> str:
 _KERNEL = re.compile(r"^[0-9a-f]+ <(\S+)>:$")
 _AGPR_MFMA = re.compile(r"v_mfma\S* a\[")
 _ANY_AGPR = re.compile(r"\ba\d+\b|\ba\[\d+:\d+\]")
-_COMPILER_AGPR = re.compile(r"v_accvgpr_write_b32 a\d+, v\d+|v_accvgpr_mov_b32|scratch_")
+# The only instructions that may name an AGPR in a kernel whose accumulators
+# the inline asm holds: the asm's MFMA on an accumulator tile (destination and
+# C operand the same a[n:n+3]), its zeroing write and its read into a VGPR.
+_ASM_MFMA = re.compile(r"^v_mfma\S*\s+(a\[\d+:\d+\]),\s*v\[\d+:\d+\],\s*v\[\d+:\d+\],\s*(a\[\d+:\d+\])")
+_ASM_ZERO = re.compile(r"^v_accvgpr_write_b32\s+a\d+,\s*0\s*$")
+_ASM_READ = re.compile(r"^v_accvgpr_read_b32\s+v\d+,\s*a\d+\s*$")
+
+
+def _asm_agpr_form(insn: str) -> bool:
+    """Whether an instruction that names an AGPR is one of the accumulator
+    asm's own forms."""
+    m = _ASM_MFMA.match(insn)
+    if m:
+        # the MFMA's remaining operands (block-scale words, modifiers) name no AGPR
+        rest = insn[m.end():]
+        return m.group(1) == m.group(2) and not _ANY_AGPR.search(rest)
+    return bool(_ASM_ZERO.match(insn) or _ASM_READ.match(insn))
 
 
 def check_accumulator_isolation(obj: str, tmp: str) -> int:
@@ -80,7 +98,13 @@ def check_accumulator_isolation(obj: str, tmp: str) -> int:
                 raise RuntimeError(f"{obj}: function {name} uses AGPRs: {bad[:4]}")
             continue
         checked += 1
-        bad = [l.strip() for l in body if _COMPILER_AGPR.search(l)]
+        bad = []
+        for line in body:
+            insn = line.split("//")[0].strip()
+            if "scratch_" in insn:
+                bad.append(insn)
+            elif _ANY_AGPR.search(insn) and not _asm_agpr_form(insn):
+                bad.append(insn)
         if bad:
             raise RuntimeError(f"{obj}: kernel {name} has compiler-placed AGPR or scratch "
                                f"accesses next to the asm-held accumulators: {bad[:4]}")

@@ -919,6 +919,7 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
     // MX: block-scale words by step parity, like af: A's for the wave's
     // rows 0 .. 63 and 64 .. 127 (byte mi & 3), B's for its columns likewise
     int sa[2][2] = {}, sb[2][2] = {};
+    static_assert(!MX || (MI == 8 && NI == 8 && WTM == 128 && WTN == 128), "MX word layout");
 
     auto head = [&](auto par_tag, int kt) {
       constexpr int P = decltype(par_tag)::value;
