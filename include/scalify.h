@@ -254,6 +254,27 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
                               scalify_scaled_array* out, const scalify_matmul_opts* opts,
                               void* workspace, size_t workspace_bytes, void* stream);
 
+/* scalify_matmul for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same computation, arguments and statuses, with the workspace taken
+ * from a static array of the library instead of the caller. The library
+ * holds one such array of 256 + 32 MiB bytes on every GPU it runs on, from
+ * the first call with that GPU current until the process ends; this call
+ * allocates nothing itself. A call whose workspace size
+ * (scalify_matmul_workspace_size_opts) exceeds 256 + 32 MiB returns
+ * SCALIFY_ERR_WORKSPACE and enqueues nothing: DELAYED calls fit at any size
+ * (header only); NONE / AMAX calls fit while M x round_up(N, 16) x (2 for
+ * FP8 outputs, 4 for FP16 outputs and fused / channel / block-scaled calls)
+ * <= 32 MiB, e.g. 4096 x 4096 FP8 outputs. Every call on one GPU shares its
+ * array: calls that may overlap on one GPU (other streams, other host
+ * threads) race and must be ordered by the caller. `stream` must belong to
+ * the current GPU. The array keeps the last call's contents; each call
+ * clears what it needs cleared. SCALIFY_ERR_HIP also when the array's
+ * address cannot be obtained. */
+scalify_status scalify_matmul_noalloc(const scalify_scaled_array* a,
+                                      const scalify_scaled_array* b, scalify_scaled_array* out,
+                                      const scalify_matmul_opts* opts, void* stream);
+
 /* Bytes of device workspace scalify_rescale needs (a 256-byte header). */
 size_t scalify_rescale_workspace_size(int64_t n);
 

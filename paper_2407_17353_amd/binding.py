@@ -58,7 +58,8 @@ EXPORTED = ("scalify_matmul_scale_log2", "scalify_matmul_workspace_size",
             "scalify_rescale_workspace_size", "scalify_rescale", "scalify_cast",
             "scalify_set_scaling", "scalify_status_string", "scalify_layernorm_fwd",
             "scalify_layernorm_bwd_workspace_size", "scalify_layernorm_bwd",
-            "scalify_mx_packed_bytes", "scalify_mx_pack_block_scales")
+            "scalify_mx_packed_bytes", "scalify_mx_pack_block_scales",
+            "scalify_matmul_noalloc")
 
 _lib = None
 
@@ -87,6 +88,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.scalify_matmul.argtypes = [P(CScaledArray), P(CScaledArray), P(CScaledArray),
                                    P(CMatmulOpts), vp, ctypes.c_size_t, vp]
     lib.scalify_matmul.restype = ctypes.c_int
+    lib.scalify_matmul_noalloc.argtypes = [P(CScaledArray), P(CScaledArray), P(CScaledArray),
+                                           P(CMatmulOpts), vp]
+    lib.scalify_matmul_noalloc.restype = ctypes.c_int
     lib.scalify_rescale_workspace_size.argtypes = [i64]
     lib.scalify_rescale_workspace_size.restype = ctypes.c_size_t
     lib.scalify_rescale.argtypes = [P(CScaledArray), P(CScaledArray), i32, i32, i32, vp,
@@ -229,6 +233,47 @@ def scalify_matmul(a: ScaledArray, b: ScaledArray, out: ScaledArray, *, rescale:
     lib = load_library()
     M, _ = a.shape
     _, N = b.shape
+    opts, keep = _matmul_opts(a, out, rescale, target_log2, saturate, acc_out, amax_out, amax_in,
+                              residual, activation, pre_out, a_channel_scale, b_channel_scale,
+                              a_block_scale, b_block_scale, stream, events)
+    if ws is None:
+        ws = workspace(lib.scalify_matmul_workspace_size_opts(M, N, ctypes.byref(opts)),
+                       a.data.device)
+    ca, cb, co = a.c_struct(), b.c_struct(), out.c_struct()
+    st = lib.scalify_matmul(ctypes.byref(ca), ctypes.byref(cb), ctypes.byref(co), ctypes.byref(opts),
+                            ws.data_ptr(), ws.numel(), _stream_handle(stream))
+    _check(st, "scalify_matmul")
+
+
+def scalify_matmul_noalloc(a: ScaledArray, b: ScaledArray, out: ScaledArray, *,
+                           rescale: int = RESCALE_AMAX, target_log2: int = 0,
+                           saturate: bool = True, acc_out: torch.Tensor = None,
+                           amax_out: torch.Tensor = None, amax_in: torch.Tensor = None,
+                           residual: "ScaledArray" = None, activation: int = ACT_NONE,
+                           pre_out: torch.Tensor = None, a_channel_scale: torch.Tensor = None,
+                           b_channel_scale: torch.Tensor = None,
+                           a_block_scale: torch.Tensor = None, b_block_scale: torch.Tensor = None,
+                           stream=None, events=None) -> None:
+    """scalify_matmul with the library's static workspace (no allocation by
+    the library or by this binding); see scalify_matmul_noalloc in
+    include/scalify.h for its size limit and its sharing rules."""
+    lib = load_library()
+    opts, keep = _matmul_opts(a, out, rescale, target_log2, saturate, acc_out, amax_out, amax_in,
+                              residual, activation, pre_out, a_channel_scale, b_channel_scale,
+                              a_block_scale, b_block_scale, stream, events)
+    ca, cb, co = a.c_struct(), b.c_struct(), out.c_struct()
+    st = lib.scalify_matmul_noalloc(ctypes.byref(ca), ctypes.byref(cb), ctypes.byref(co),
+                                    ctypes.byref(opts), _stream_handle(stream))
+    _check(st, "scalify_matmul_noalloc")
+
+
+def _matmul_opts(a, out, rescale, target_log2, saturate, acc_out, amax_out, amax_in, residual,
+                 activation, pre_out, a_channel_scale, b_channel_scale, a_block_scale,
+                 b_block_scale, stream, events):
+    """The scalify_matmul_opts struct of a call, and the ctypes objects it
+    points to (kept alive by the caller until the call returns)."""
+    M, K = a.shape
+    N = out.shape[1]
     ev_arr = None
     if events is not None:
         for e in events:
@@ -247,18 +292,12 @@ def scalify_matmul(a: ScaledArray, b: ScaledArray, out: ScaledArray, *, rescale:
                        b_block_scale.data_ptr() if b_block_scale is not None else None)
     for t, rows in ((a_block_scale, M), (b_block_scale, N)):
         if t is not None and (t.dtype != torch.uint8 or not t.is_contiguous() or
-                              t.numel() != scalify_mx_packed_bytes(rows, a.shape[1])):
+                              t.numel() != scalify_mx_packed_bytes(rows, K)):
             raise ValueError("block scales: packed by scalify_mx_pack_block_scales")
     cr = residual.c_struct() if residual is not None else None
     if cr is not None:
         opts.residual = ctypes.pointer(cr)
-    if ws is None:
-        ws = workspace(lib.scalify_matmul_workspace_size_opts(M, N, ctypes.byref(opts)),
-                       a.data.device)
-    ca, cb, co = a.c_struct(), b.c_struct(), out.c_struct()
-    st = lib.scalify_matmul(ctypes.byref(ca), ctypes.byref(cb), ctypes.byref(co), ctypes.byref(opts),
-                            ws.data_ptr(), ws.numel(), _stream_handle(stream))
-    _check(st, "scalify_matmul")
+    return opts, (ev_arr, cr)
 
 
 def scalify_rescale(x: ScaledArray, out: ScaledArray, *, mode: int = RESCALE_AMAX, target_log2: int = 0,

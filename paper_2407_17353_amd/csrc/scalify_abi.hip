@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "../../include/scalify.h"
 #include "kernels.h"
 #include "layernorm.h"
@@ -125,6 +127,34 @@ bool rows_conflict(const scalify_scaled_array* a, const scalify_scaled_array* b,
   const bool same = a->data == b->data && elem_bytes(a->dtype) == elem_bytes(b->dtype) &&
                     a->ld == b->ld;
   return a0 < b1 && b0 < a1 && !same;
+}
+
+// ---- allocation-free matmul: its workspace is this file-scope device array
+// (header + pre-cast intermediate), one copy per GPU the library runs on,
+// held until the process ends. In host code `scratch` names a host-side
+// stand-in; its device address, different on every GPU, comes from
+// hipGetSymbolAddress with that GPU current and is the only form passed on.
+constexpr size_t kNoallocScratchBytes = kHeaderBytes + ((size_t)32 << 20);
+static __device__ __align__(256) uint8_t scratch[kNoallocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices];
+
+// Device address of the current GPU's scratch array (looked up on the first
+// call made with that GPU current, then kept).
+scalify_status current_scratch(void** ptr) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return SCALIFY_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr)
+      return SCALIFY_ERR_HIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return SCALIFY_OK;
 }
 
 size_t layernorm_bwd_ws(int64_t R, int64_t D) {
@@ -333,6 +363,18 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
   }
   if (ev && ev[2] && hipEventRecord(ev[2], s) != hipSuccess) return SCALIFY_ERR_HIP;
   return SCALIFY_OK;
+}
+
+scalify_status scalify_matmul_noalloc(const scalify_scaled_array* a,
+                                      const scalify_scaled_array* b, scalify_scaled_array* out,
+                                      const scalify_matmul_opts* opts, void* stream) {
+  if (!a || !b || !out || !opts) return SCALIFY_ERR_NULL;
+  // A workspace larger than the array is refused before anything is enqueued
+  // (scalify_matmul checks the other arguments first and returns their error).
+  void* ws = nullptr;
+  const scalify_status st = current_scratch(&ws);
+  if (st != SCALIFY_OK) return st;
+  return scalify_matmul(a, b, out, opts, ws, kNoallocScratchBytes, stream);
 }
 
 scalify_status scalify_rescale(const scalify_scaled_array* in, scalify_scaled_array* out,
