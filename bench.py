@@ -338,6 +338,18 @@ def main():
                      "frac": round(gemm_tflops / PEAK_FP8_TFLOPS, 4),
                      "traffic": measured_traffic()},
     }
+    # The same call forced through the single pass (one kernel: GEMM, grid
+    # barrier on the statistic, cast), for comparison with the GEMM + cast
+    # kernel pair timed above: 1024 tiles on one workgroup per CU, so the
+    # three earlier tiles of each workgroup still pass the intermediate.
+    os.environ["SCALIFY_SINGLE_PASS"] = "1"
+    r2, ws = time_case(case, args.steps, args.warmup // 2, dev, ws)
+    del os.environ["SCALIFY_SINGLE_PASS"]
+    line["single_pass_rescale"] = {
+        "value": round(flops / (r2["ms_per_step"] * 1e-3) / 1e12, 2), "unit": "TFLOP/s",
+        "ms_per_step": round(r2["ms_per_step"], 4),
+        "gemm_kernel_us": round(r2["gemm_ms"] * 1e3, 2),
+        "epilogue_cast_us": round(r2["cast_ms"] * 1e3, 2)}
     # The delayed rescale (Section 3.3) on the same workload: the statistic of
     # the previous call sets the scale, the GEMM writes the codes directly.
     rd, ws = time_case(case, args.steps, args.warmup // 2, dev, ws, mode=sc.RESCALE_DELAYED)

@@ -172,15 +172,16 @@ scalify_status scalify_mx_pack_block_scales(const uint8_t* src, int64_t rows, in
 int32_t scalify_matmul_scale_log2(int64_t K);
 
 /* Bytes of device workspace scalify_matmul needs for an M x N output with
- * the given output type and rescale mode: a 256-byte header plus, for NONE
- * and AMAX, the pre-cast intermediate (M rows of N rounded up to 16
- * elements; 2 bytes per element for FP8 outputs, 4 for FP16). DELAYED needs
- * the header only. Returns 0 for invalid arguments. */
+ * the given output type and rescale mode: a 256-byte header plus, for AMAX,
+ * the pre-cast intermediate (M rows of N rounded up to 16 elements; 2 bytes
+ * per element for FP8 outputs, 4 for FP16). DELAYED and NONE, whose output
+ * scale is known before the GEMM runs, need the header only. Returns 0 for
+ * invalid arguments. */
 size_t scalify_matmul_workspace_size(int64_t M, int64_t N, int32_t out_dtype, int32_t rescale);
 
 /* Workspace bytes of a scalify_matmul call with these options: as above, but
- * a call that fuses a residual add or an activation, has channel or MX block
- * scales, or asks for pre_out, keeps an fp32 intermediate (4 bytes per
+ * an AMAX call that fuses a residual add or an activation, has channel or MX
+ * block scales, or asks for pre_out, keeps an fp32 intermediate (4 bytes per
  * element for every output type).
  * Returns 0 for invalid arguments or a NULL opts. */
 size_t scalify_matmul_workspace_size_opts(int64_t M, int64_t N, const scalify_matmul_opts* opts);
@@ -198,7 +199,7 @@ size_t scalify_matmul_workspace_size_opts(int64_t M, int64_t N, const scalify_ma
  *         the stale scale pushes past the format's range saturate (or
  *         overflow when saturate = 0). The GEMM writes the codes directly:
  *         no intermediate, no second pass over the output.
- *   NONE: e_r = 0
+ *   NONE: e_r = 0 (the GEMM writes the codes directly, as for DELAYED)
  *   e_out = clamp(e_a + e_b + e_c + e_r, -127, 127)        (E8M0 range)
  *   out.data  = RNE(acc * 2^(e_a + e_b - e_out)) in out.dtype (saturating
  *               when opts.saturate), *out.scale = 2^e_out
@@ -249,7 +250,23 @@ size_t scalify_matmul_workspace_size_opts(int64_t M, int64_t N, const scalify_ma
  * at least scalify_matmul_workspace_size_opts(M, N, opts) bytes (for a call
  * with nothing fused: scalify_matmul_workspace_size(M, N, ...)), 256-byte aligned,
  * not shared with a concurrent call. Determinism: reruns are bit-identical.
- * M, N or K may be 0 (K = 0 gives an all-zero output). */
+ * M, N or K may be 0 (K = 0 gives an all-zero output).
+ *
+ * AMAX without a fused epilogue, on an output of at most one 256 x 256 tile
+ * per compute unit, runs as one GEMM kernel (the single pass): its
+ * workgroups hold their output tile in the matrix cores' accumulators, meet
+ * at a grid barrier on the amax statistic, and cast; the output scale and
+ * amax_out are written by that kernel. Larger outputs take the GEMM + cast
+ * kernel pair (faster there). The barrier's wait is bounded: if the grid is
+ * not co-resident on the GPU (other work occupies its compute units), the
+ * workgroups fall back to casting from the intermediate after the wait, with
+ * the same result, later. Environment (read at each call):
+ * SCALIFY_SINGLE_PASS=1 takes the single pass at any size, =0 never (it
+ * does not cover block-scaled calls with a.trans = 1 and b.trans = 0);
+ * SCALIFY_SPIN_TICKS=<n> sets the barrier's wait in ticks of the
+ * GPU's 100 MHz counter (default 20 ms plus 4 us per 128 of K; 0 exercises
+ * the fallback). SCALIFY_PERSISTENT=0 launches one workgroup per tile (and no
+ * single pass) instead of the persistent grid. */
 scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scaled_array* b,
                               scalify_scaled_array* out, const scalify_matmul_opts* opts,
                               void* workspace, size_t workspace_bytes, void* stream);
@@ -262,8 +279,8 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
  * the first call with that GPU current until the process ends; this call
  * allocates nothing itself. A call whose workspace size
  * (scalify_matmul_workspace_size_opts) exceeds 256 + 32 MiB returns
- * SCALIFY_ERR_WORKSPACE and enqueues nothing: DELAYED calls fit at any size
- * (header only); NONE / AMAX calls fit while M x round_up(N, 16) x (2 for
+ * SCALIFY_ERR_WORKSPACE and enqueues nothing: DELAYED and NONE calls fit at
+ * any size (header only); AMAX calls fit while M x round_up(N, 16) x (2 for
  * FP8 outputs, 4 for FP16 outputs and fused / channel / block-scaled calls)
  * <= 32 MiB, e.g. 4096 x 4096 FP8 outputs. Every call on one GPU shares its
  * array: calls that may overlap on one GPU (other streams, other host

@@ -9,7 +9,8 @@
 //     magnitude keys (no decode in the hot loop);
 //   * elementwise: rebalance / set_scaling / cast of a ScaledArray's data.
 // Every kernel moves 16 elements per thread per iteration with 128-bit
-// loads and stores and walks the array with a grid-stride loop.
+// loads; the cast kernel walks rows of the intermediate, the amax and
+// elementwise kernels walk 1024-element blocks (layout below).
 #include "codec.h"
 #include "ew_util.h"
 #include "kernels.h"
@@ -33,7 +34,8 @@ hipError_t launch_prologue(uint32_t* hdr, const float* s0, const float* s1, hipS
 // Matmul prologue: the scale exponent e_w of the pre-cast value (scaled add
 // rule of Algorithm 3 with a residual) and, for the delayed rescale
 // (Section 3.3), the output scale from the statistic an earlier call
-// recorded, so that the GEMM can cast directly.
+// recorded, or without a rescale the propagated scale itself, so that the
+// GEMM can cast directly; clears the statistic and the single-pass barrier.
 __global__ void matmul_prologue_kernel(uint32_t* hdr, MatmulPrologue q) {
   if (threadIdx.x == 0) {
     const int e_ab = pow2_exponent(q.s0) + pow2_exponent(q.s1);
@@ -49,8 +51,10 @@ __global__ void matmul_prologue_kernel(uint32_t* hdr, MatmulPrologue q) {
     }
     hdr[0] = 0u;
     hdr[1] = (uint32_t)e_w;
-    if (q.delayed) {
-      const uint32_t stat = __float_as_uint(*q.amax_in) & 0x7FFFFFFFu;  // |statistic|
+    hdr[5] = hdr[6] = hdr[7] = 0u;
+    if (q.direct) {
+      // |statistic| of an earlier call (delayed rescale), or none (e_r = 0)
+      const uint32_t stat = q.amax_in ? __float_as_uint(*q.amax_in) & 0x7FFFFFFFu : 0u;
       const int e_r = rescale_exponent(stat, q.target);  // 0 for 0, Inf, NaN
       const int e_out = clamp_e8m0(e_w + e_cc + e_r);
       hdr[2] = (uint32_t)(e_out - e_w);
@@ -151,12 +155,6 @@ __global__ __launch_bounds__(EW_THREADS) void epilogue_cast_kernel(EpilogueParam
   }
 }
 
-static int grid_for(int64_t work) {
-  int64_t b = (work + EW_THREADS - 1) / EW_THREADS;
-  if (b < 1) b = 1;
-  if (b > 8192) b = 8192;
-  return (int)b;
-}
 
 // 16-bit intermediates above this size no longer sit in the 256 MiB MALL
 // after the GEMM has written them. Measured (cast kernel alone): nontemporal
@@ -196,26 +194,86 @@ hipError_t launch_epilogue_cast(const EpilogueParams& p, int inter32, int out_dt
   return hipGetLastError();
 }
 
-// ---------------------------------------------------------------- amax
+// ---------------------------------------------------------------- amax / elementwise
+//
+// Block layout of the streaming kernels: a block is 1024 consecutive
+// elements, read by one wave as W 16-byte words per lane (W = 4 for fp32, 2
+// for FP16, 1 for FP8): word w of lane l is word 64 w + l of the block, so
+// every load instruction of the wave reads 1 KiB of consecutive bytes, and
+// a lane's 16 elements are the EPW = 16 / W elements of each of its words.
+// Waves walk the blocks with a stride of the whole grid, two blocks per
+// iteration (2 W loads in flight per lane); the last partial block is done
+// element by element by the first workgroup.
+constexpr int EW_GRID = 2048;  // workgroups of 4 waves: 8 per CU
+
+template <int F>
+struct BlockLayout {
+  static constexpr int ESZ = F == kF32 ? 4 : (F == kF16 ? 2 : 1);
+  static constexpr int EPW = 16 / ESZ;  // elements per 16-byte word
+  static constexpr int W = 16 / EPW;    // words per lane and block
+};
+
+// Load block b's words of this lane (raw 16-byte words).
+template <int F>
+__device__ __forceinline__ void load_block(const void* in, int64_t b, int lane,
+                                           u4 (&w)[BlockLayout<F>::W]) {
+  constexpr int W = BlockLayout<F>::W;
+  const u4* q = (const u4*)in + b * (64 * W) + lane;
+#pragma unroll
+  for (int k = 0; k < W; ++k) w[k] = q[64 * k];
+}
+
+// The lane's 16 elements of a block as codes (or fp32 bits), word by word.
+template <int F>
+__device__ __forceinline__ void unpack_block(const u4 (&w)[BlockLayout<F>::W], uint32_t (&c)[16]) {
+  constexpr int W = BlockLayout<F>::W, EPW = BlockLayout<F>::EPW;
+#pragma unroll
+  for (int k = 0; k < W; ++k)
+#pragma unroll
+    for (int i = 0; i < EPW; ++i) {
+      const uint32_t word = w[k][i * 4 / EPW];
+      if constexpr (F == kF32) c[k * EPW + i] = word;
+      else if constexpr (F == kF16) c[k * EPW + i] = (word >> (16 * (i & 1))) & 0xFFFFu;
+      else c[k * EPW + i] = (word >> (8 * (i & 3))) & 0xFFu;
+    }
+}
 
 template <int F>
 __global__ __launch_bounds__(EW_THREADS) void amax_kernel(const void* in, int64_t n,
                                                            uint32_t* hdr) {
+  using L = BlockLayout<F>;
   __shared__ uint32_t red[EW_THREADS / 64];
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (int64_t)blockIdx.x * (EW_THREADS / 64) + (threadIdx.x >> 6);
+  const int64_t waves = (int64_t)gridDim.x * (EW_THREADS / 64);
+  const int64_t nb = n / 1024;
   uint32_t kmax = 0;
-  const int64_t nv = n / 16;
-  for (int64_t v = (int64_t)blockIdx.x * EW_THREADS + threadIdx.x; v < nv;
-       v += (int64_t)gridDim.x * EW_THREADS) {
+  int64_t b = wave;
+  for (; b + waves < nb; b += 2 * waves) {
+    u4 w0[L::W], w1[L::W];
+    load_block<F>(in, b, lane, w0);
+    load_block<F>(in, b + waves, lane, w1);
     uint32_t c[16];
-    load16<F>(in, v * 16, c);
+    unpack_block<F>(w0, c);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) kmax = max(kmax, magnitude_key<F>(c[i]));
+    unpack_block<F>(w1, c);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) kmax = max(kmax, magnitude_key<F>(c[i]));
+  }
+  if (b < nb) {
+    u4 w0[L::W];
+    load_block<F>(in, b, lane, w0);
+    uint32_t c[16];
+    unpack_block<F>(w0, c);
 #pragma unroll
     for (int i = 0; i < 16; ++i) kmax = max(kmax, magnitude_key<F>(c[i]));
   }
   if (blockIdx.x == 0)
-    for (int64_t e = nv * 16 + threadIdx.x; e < n; e += EW_THREADS)
+    for (int64_t e = nb * 1024 + threadIdx.x; e < n; e += EW_THREADS)
       kmax = max(kmax, magnitude_key<F>(load1<F>(in, e)));
   for (int off = 32; off > 0; off >>= 1) kmax = max(kmax, (uint32_t)__shfl_xor((int)kmax, off, 64));
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = kmax;
+  if (lane == 0) red[threadIdx.x >> 6] = kmax;
   __syncthreads();
   if (threadIdx.x == 0) {
     uint32_t k = red[0];
@@ -224,8 +282,16 @@ __global__ __launch_bounds__(EW_THREADS) void amax_kernel(const void* in, int64_
   }
 }
 
+static int ew_grid(int64_t n) {
+  const int64_t waves = (n + 1023) / 1024;  // one wave per block at most
+  int64_t g = (waves + EW_THREADS / 64 - 1) / (EW_THREADS / 64);
+  if (g < 1) g = 1;
+  if (g > EW_GRID) g = EW_GRID;
+  return (int)g;
+}
+
 hipError_t launch_amax(const void* in, int in_dtype, int64_t n, uint32_t* hdr, hipStream_t s) {
-  const dim3 g(grid_for(n / 16)), b(EW_THREADS);
+  const dim3 g(ew_grid(n)), b(EW_THREADS);
   switch (in_dtype) {
     case kE4M3: hipLaunchKernelGGL((amax_kernel<kE4M3>), g, b, 0, s, in, n, hdr); break;
     case kE5M2: hipLaunchKernelGGL((amax_kernel<kE5M2>), g, b, 0, s, in, n, hdr); break;
@@ -237,8 +303,32 @@ hipError_t launch_amax(const void* in, int in_dtype, int64_t n, uint32_t* hdr, h
 
 // ---------------------------------------------------------------- rescale / cast / set_scaling
 
+// Store the codes of a lane's 16 block elements (words w as encode16 packs
+// them: FP8 4 codes per word, FP16 2) at their elements: the EPW codes of
+// input word k go to element 64 k + lane (in units of EPW elements) of the
+// block, as one store of EPW * (1 or 2) bytes.
+template <int INF, int OUTF>
+__device__ __forceinline__ void store_block(void* out, int64_t b, int lane, const uint32_t (&w)[8]) {
+  constexpr int W = BlockLayout<INF>::W, EPW = BlockLayout<INF>::EPW;
+  constexpr int OB = OUTF == kF16 ? 2 : 1;  // output bytes per element
+  constexpr int WPW = EPW * OB / 4;         // packed 32-bit words per input word
+  uint8_t* base = (uint8_t*)out + (b * 1024) * OB;
+#pragma unroll
+  for (int k = 0; k < W; ++k) {
+    uint8_t* q = base + (int64_t)(64 * k + lane) * EPW * OB;
+    if constexpr (WPW == 1) *(uint32_t*)q = w[k];
+    else if constexpr (WPW == 2) *(uint2*)q = uint2{w[2 * k], w[2 * k + 1]};
+    else if constexpr (WPW == 4) *(u4*)q = u4{w[4 * k], w[4 * k + 1], w[4 * k + 2], w[4 * k + 3]};
+    else {
+      *(u4*)q = u4{w[0], w[1], w[2], w[3]};
+      *(u4*)(q + 16) = u4{w[4], w[5], w[6], w[7]};
+    }
+  }
+}
+
 template <int INF, int OUTF>
 __global__ __launch_bounds__(EW_THREADS) void elementwise_kernel(ElemParams p) {
+  using L = BlockLayout<INF>;
   int shift = 0, e_out = 0;
   if (p.rule != RULE_COPY) {
     const int e_in = p.hdr ? (int)p.hdr[1] : pow2_exponent(p.in_scale);
@@ -254,19 +344,34 @@ __global__ __launch_bounds__(EW_THREADS) void elementwise_kernel(ElemParams p) {
     if (p.rule == RULE_COPY) *p.out_scale = p.in_scale ? *p.in_scale : 1.0f;
     else *p.out_scale = pow2_float(e_out);
   }
-  const int64_t nv = p.n / 16;
-  for (int64_t v = (int64_t)blockIdx.x * EW_THREADS + threadIdx.x; v < nv;
-       v += (int64_t)gridDim.x * EW_THREADS) {
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (int64_t)blockIdx.x * (EW_THREADS / 64) + (threadIdx.x >> 6);
+  const int64_t waves = (int64_t)gridDim.x * (EW_THREADS / 64);
+  const int64_t nb = p.n / 1024;
+  auto cast_block = [&](const u4 (&w)[L::W], int64_t b) {
     uint32_t c[16];
-    load16<INF>(p.in, v * 16, c);
+    unpack_block<INF>(w, c);
 #pragma unroll
     for (int i = 0; i < 16; ++i) c[i] = to_bits<INF>(c[i]);
-    uint32_t w[8];
-    encode16<OUTF>(c, shift, scale, fast, sat, w);
-    store_words16<OUTF>(p.out, v * 16, w);
+    uint32_t o[8];
+    encode16<OUTF>(c, shift, scale, fast, sat, o);
+    store_block<INF, OUTF>(p.out, b, lane, o);
+  };
+  int64_t b = wave;
+  for (; b + waves < nb; b += 2 * waves) {
+    u4 w0[L::W], w1[L::W];
+    load_block<INF>(p.in, b, lane, w0);
+    load_block<INF>(p.in, b + waves, lane, w1);
+    cast_block(w0, b);
+    cast_block(w1, b + waves);
+  }
+  if (b < nb) {
+    u4 w0[L::W];
+    load_block<INF>(p.in, b, lane, w0);
+    cast_block(w0, b);
   }
   if (blockIdx.x == 0)
-    for (int64_t e = nv * 16 + threadIdx.x; e < p.n; e += EW_THREADS)
+    for (int64_t e = nb * 1024 + threadIdx.x; e < p.n; e += EW_THREADS)
       store1<OUTF>(p.out, e, cast_bits<OUTF>(to_bits<INF>(load1<INF>(p.in, e)), shift, sat));
 }
 
@@ -278,7 +383,7 @@ static void launch_elem_out(const ElemParams& p, int out_dtype, dim3 g, dim3 b, 
 }
 
 hipError_t launch_elementwise(const ElemParams& p, int in_dtype, int out_dtype, hipStream_t s) {
-  const dim3 g(grid_for(p.n / 16)), b(EW_THREADS);
+  const dim3 g(ew_grid(p.n)), b(EW_THREADS);
   switch (in_dtype) {
     case kE4M3: launch_elem_out<kE4M3>(p, out_dtype, g, b, s); break;
     case kE5M2: launch_elem_out<kE5M2>(p, out_dtype, g, b, s); break;

@@ -85,14 +85,14 @@ __device__ __forceinline__ float decode_hw(uint32_t c) {
 // Exact integer casts of 4 values, out of line: they run only for chunks
 // that hold a NaN or for shifts outside the hardware conversions' window.
 template <int OUTF>
-static __device__ __attribute__((noinline)) uint32_t cast4_exact_fp8(uint32_t u0, uint32_t u1,
+[[maybe_unused]] static __device__ __attribute__((noinline)) uint32_t cast4_exact_fp8(uint32_t u0, uint32_t u1,
                                                                      uint32_t u2, uint32_t u3,
                                                                      int shift, bool sat) {
   return cast_bits<OUTF>(u0, shift, sat) | (cast_bits<OUTF>(u1, shift, sat) << 8) |
          (cast_bits<OUTF>(u2, shift, sat) << 16) | (cast_bits<OUTF>(u3, shift, sat) << 24);
 }
 
-static __device__ __attribute__((noinline)) uint32_t cast2_exact_f16(uint32_t u0, uint32_t u1,
+[[maybe_unused]] static __device__ __attribute__((noinline)) uint32_t cast2_exact_f16(uint32_t u0, uint32_t u1,
                                                                      int shift, bool sat) {
   return cast_bits<kF16>(u0, shift, sat) | (cast_bits<kF16>(u1, shift, sat) << 16);
 }

@@ -1,22 +1,56 @@
 // Dispatch of the scaled FP8 GEMM over the four storage orders of A and B.
-#include "gemm_kernel.h"
+#include "gemm4_kernel.h"
 
 namespace scalify {
 
-hipError_t launch_gemm(const GemmParams& p, bool a_mn, bool b_kc, int fa, int fb, int epi,
+int gemm4_grid(int tiles) {
+  constexpr int kMaxDevices = 64;
+  static int cus[kMaxDevices];  // CUs per device, looked up once (a benign race)
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) dev = -1;
+  int n = dev >= 0 ? cus[dev] : 0;
+  if (n <= 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev < 0 ? 0 : dev) !=
+            hipSuccess || n <= 0)
+      n = 256;
+    if (dev >= 0) cus[dev] = n;
+  }
+  return tiles < n ? tiles : n;
+}
+
+hipError_t launch_gemm(const GemmParams& p_in, bool a_mn, bool b_kc, int fa, int fb, int epi,
                        bool fuse, hipStream_t s) {
-  if (p.tiles_m * p.tiles_n == 0) return hipSuccess;
+  if (p_in.tiles_m * p_in.tiles_n == 0) return hipSuccess;
+  GemmParams p = p_in;
+  p.epi = epi;
   if (p.mx_a) {
-    if (!a_mn && b_kc) return launch_layout_mx<false, true>(p, fa, fb, epi, s);
-    if (!a_mn && !b_kc) return launch_layout_mx<false, false>(p, fa, fb, epi, s);
-    if (a_mn && b_kc) return launch_layout_mx<true, true>(p, fa, fb, epi, s);
-    return launch_layout_mx<true, false>(p, fa, fb, epi, s);
+    if (mx_on_8_waves(a_mn, b_kc)) return launch_layout_mx<true, false>(p, fa, fb, epi, s);
+    if (!p.single_pass) {
+      if (!a_mn && b_kc) return launch_layout_mx<false, true>(p, fa, fb, epi, s);
+      if (!a_mn && !b_kc) return launch_layout_mx<false, false>(p, fa, fb, epi, s);
+      return launch_layout_mx<true, true>(p, fa, fb, epi, s);
+    }
+    if (!a_mn && b_kc) return launch_layout_mx_sp<false, true>(p, fa, fb, epi, s);
+    if (!a_mn && !b_kc) return launch_layout_mx_sp<false, false>(p, fa, fb, epi, s);
+    return launch_layout_mx_sp<true, true>(p, fa, fb, epi, s);
   }
   if (fuse) {
     if (!a_mn && b_kc) return launch_layout<false, true, true>(p, fa, fb, epi, s);
     if (!a_mn && !b_kc) return launch_layout<false, false, true>(p, fa, fb, epi, s);
     if (a_mn && b_kc) return launch_layout<true, true, true>(p, fa, fb, epi, s);
     return launch_layout<true, false, true>(p, fa, fb, epi, s);
+  }
+  if (epi == EPI_DIRECT) {
+    if (!a_mn && b_kc) return launch_layout_direct<false, true>(p, fa, fb, epi, s);
+    if (!a_mn && !b_kc) return launch_layout_direct<false, false>(p, fa, fb, epi, s);
+    if (a_mn && b_kc) return launch_layout_direct<true, true>(p, fa, fb, epi, s);
+    return launch_layout_direct<true, false>(p, fa, fb, epi, s);
+  }
+  if (p.single_pass) {
+    if (!a_mn && b_kc) return launch_layout_sp<false, true>(p, fa, fb, epi, s);
+    if (!a_mn && !b_kc) return launch_layout_sp<false, false>(p, fa, fb, epi, s);
+    if (a_mn && b_kc) return launch_layout_sp<true, true>(p, fa, fb, epi, s);
+    return launch_layout_sp<true, false>(p, fa, fb, epi, s);
   }
   if (!a_mn && b_kc) return launch_layout<false, true, false>(p, fa, fb, epi, s);
   if (!a_mn && !b_kc) return launch_layout<false, false, false>(p, fa, fb, epi, s);

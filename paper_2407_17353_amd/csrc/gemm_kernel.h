@@ -189,9 +189,12 @@ __device__ __forceinline__ TileLoader make_loader(uint32_t ld, int wave, int lan
 // through the buffer range check; KC chunks that start at or beyond K are
 // sent out of range too, and a chunk straddling K is trimmed by
 // zero_tail_kc.
+// ok = false (no tile left to load: the persistent kernel's last steps)
+// sends the whole load out of range.
 template <bool KC, int BPW>
 __device__ __forceinline__ void issue_block(v4i rsrc, const TileLoader& L, uint32_t ld, int row0,
-                                            int k0, int K, uint8_t* lds, int wave, int q) {
+                                            int k0, int K, uint8_t* lds, int wave, int q,
+                                            bool ok = true) {
   const int blk = wave * BPW + q;
   uint32_t off;
   if (KC) {
@@ -200,7 +203,25 @@ __device__ __forceinline__ void issue_block(v4i rsrc, const TileLoader& L, uint3
   } else {
     off = (uint32_t)(k0 + blk * 4) * ld + (uint32_t)row0 + L.lane_off[q & 1];
   }
+  if (!ok) off = (uint32_t)rsrc.z;
   load_lds16(rsrc, off, lds + blk * 1024);
+}
+
+// Origin of output tile t (0 .. tiles_m * tiles_n - 1): ids are dealt
+// round-robin over the 8 XCDs, so when the tile count is a multiple of 8,
+// id t is remapped so that each XCD walks a contiguous range of tiles; the
+// range is walked in groups 4 tile-rows high, so that the tiles that run
+// together on one XCD share A and B panels in its L2.
+__device__ __forceinline__ void tile_origin(int t, int tiles_m, int tiles_n, int& m0, int& n0) {
+  const int T = tiles_m * tiles_n;
+  if ((T & 7) == 0) t = (t & 7) * (T >> 3) + (t >> 3);
+  constexpr int G = 4;
+  const int group = t / (G * tiles_n);
+  const int first_m = group * G;
+  const int gm = min(tiles_m - first_m, G);
+  const int in_group = t - group * G * tiles_n;
+  m0 = (first_m + in_group % gm) * BM;
+  n0 = (in_group / gm) * BN;
 }
 
 // KC tiles when K is not a multiple of 16: zero the bytes k >= krem of the
@@ -657,10 +678,10 @@ __device__ __forceinline__ void activate(v4f (&acc)[MI_][NI_], int e_w) {
 template <bool A_MN, bool B_KC, int FA, int FB, int EPI, bool FUSE, int NW, bool CH = false,
           bool MX = false>
 __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
-  static_assert(NW == 8 || (NW == 4 && !FUSE), "the fused epilogue runs on the 8-wave kernel");
+  static_assert(NW == 8, "two waves per SIMD (the 4-wave arrangement is gemm4_kernel)");
   static_assert(FUSE || !CH, "channel scales are part of the fused epilogue");
-  static_assert(!MX || (!FUSE && (EPI == EPI_INTER32 || (EPI == EPI_DIRECT && NW == 8))),
-                "block scales: plain epilogue, fp32 intermediate or direct cast (8 waves)");
+  static_assert(!MX || (!FUSE && (EPI == EPI_INTER32 || EPI == EPI_DIRECT)),
+                "block scales: plain epilogue, fp32 intermediate or direct cast");
   using C = WaveCfg<NW>;
   constexpr int WAVES = C::WAVES, WAVES_N = C::WAVES_N, WTM = C::WTM, WTN = C::WTN;
   constexpr int MI = C::MI, NI = C::NI, BPW = C::BPW, LOADS_PER_STEP = C::LOADS_PER_STEP;
@@ -674,17 +695,8 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
-  // ---- tile id: XCD-contiguous ranges, then 4-row grouped order
-  const int T = p.tiles_m * p.tiles_n;
-  int t = blockIdx.x;
-  if ((T & 7) == 0) t = (t & 7) * (T >> 3) + (t >> 3);
-  const int G = 4;
-  const int group = t / (G * p.tiles_n);
-  const int first_m = group * G;
-  const int gm = min(p.tiles_m - first_m, G);
-  const int in_group = t - group * G * p.tiles_n;
-  const int m0 = (first_m + in_group % gm) * BM;
-  const int n0 = (in_group / gm) * BN;
+  int m0, n0;
+  tile_origin(blockIdx.x, p.tiles_m, p.tiles_n, m0, n0);
 
   const int M = p.M, N = p.N, K = p.K;
   const int KT = (K + BK - 1) / BK;
@@ -756,16 +768,11 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
     return *(const int*)(sS + stage * 2048 + half * 1024 + 256 * j + 4 * lane);
   };
 
-  v4f acc[MI][NI];  // NW = 8 (NW = 4: AccTile)
-  if constexpr (NW == 8) {
+  v4f acc[MI][NI];
 #pragma unroll
-    for (int i = 0; i < MI; ++i)
+  for (int i = 0; i < MI; ++i)
 #pragma unroll
-      for (int j = 0; j < NI; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
-  } else {
-    static_for<0, MI * NI>([&](auto I) { AccTile<decltype(I)::value>::zero(); });
-    mfma_drain();
-  }
+    for (int j = 0; j < NI; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
 
   const int wm = (wave / WAVES_N) * WTM;  // wave sub-tile
   const int wn = (wave % WAVES_N) * WTN;
@@ -775,7 +782,7 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
   using T_ = std::true_type;
   using F_ = std::false_type;
 
-  if constexpr (NW == 8) {
+  {
     v8i a[MI];   // A fragments of the step
     v8i bq[3];   // B fragments: in use and up to two groups ahead
     // MX: this lane's block-scale words of the step: A's for the wave's 64
@@ -882,161 +889,6 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
     for (; kt + 2 < KT; ++kt) step(T_{}, T_{}, kt);
     if (kt + 1 < KT) step(F_{}, T_{}, kt++);
     if (kt < KT) step(F_{}, F_{}, kt);
-  } else {
-    // One wave per SIMD: every B fragment of a step in a register buffer of
-    // its own (bf[ni] for column group ni), A fragments double-buffered by
-    // step parity (af[kt & 1]). Two barriers per step spread the step's 16
-    // loads over most of it (the texture address path accepts about one
-    // 1 KiB load per 16 cycles per CU, so loads issued in a burst stall the
-    // wave's instruction stream and with it the matrix core):
-    //   head(kt), column groups 0 .. H - 1, which also reads the B
-    //     fragments of groups 2 .. NI - 1, one LDS read after each MFMA;
-    //     barrier X after group 0 (every wave has read step kt's A
-    //     fragments, in the previous tail), then the A loads of step kt + 2
-    //     into this step's A stage, spread over groups 1 .. H - 1;
-    //     barrier Y at its end (every wave has read step kt's B fragments,
-    //     and step kt + 1 has landed: only the A loads of step kt + 2 may
-    //     still be in flight);
-    //   tail(kt), groups H .. NI - 1 row block by row block, with the B
-    //     loads of step kt + 2 into this step's B stage and the reads of
-    //     step kt + 1's A fragments (into the other buffer) and B fragments
-    //     0 and 1, all spread over its MFMAs.
-    // The loop runs tail(kt) + head(kt + 1), unrolled by two for the parity
-    // of the A buffers. Every step has the same shape: loads of steps >= KT
-    // are range-checked to zeros and fragment reads of step KT are never
-    // used, which keeps one copy of the loop body. Program order is issue
-    // order (AccTile MFMAs are volatile asm), so the interleave is written
-    // out; the waits at the barriers are explicit (outstanding loads counted
-    // in issue order, which is also the order in which they complete).
-    constexpr int H = 6;
-    static_assert(H >= 3 && H < NI && (NI - 2) * DSB <= H * MI, "head too short for its B reads");
-    constexpr int TS = (NI - H) * MI;          // MFMAs of the tail
-    constexpr int AS = (H - 1) * MI;           // MFMAs of the head after barrier X
-    constexpr int BP = 2 * DSB;                // LDS reads of the next step's B fragments 0, 1
-    constexpr int RX = MI < (NI - 2) * DSB ? MI : (NI - 2) * DSB;  // B reads issued before X
-    v8i af[2][MI];
-    v8i bf[NI];
-    // MX: block-scale words by step parity, like af: A's for the wave's
-    // rows 0 .. 63 and 64 .. 127 (byte mi & 3), B's for its columns likewise
-    int sa[2][2] = {}, sb[2][2] = {};
-    static_assert(!MX || (MI == 8 && NI == 8 && WTM == 128 && WTN == 128), "MX word layout");
-
-    auto head = [&](auto par_tag, int kt) {
-      constexpr int P = decltype(par_tag)::value;
-      const bool odd = kt & 1;
-      uint8_t* cA = odd ? sA1 : sA0;
-      uint8_t* cB = odd ? sB1 : sB0;
-      static_for<0, H * MI>([&](auto I) {
-        constexpr int i = decltype(I)::value;
-        constexpr int ni = i / MI, mi = i % MI;
-        if constexpr (MX)
-          AccTile<mi * NI + ni>::template mfma_mx<FA, FB, ni & 3, mi & 3>(
-              bf[ni], af[P][mi], sb[P][ni >> 2], sa[P][mi >> 2]);
-        else
-          AccTile<mi * NI + ni>::template mfma<FA, FB>(bf[ni], af[P][mi]);
-        if constexpr (i < (NI - 2) * DSB) {
-          constexpr int g = 2 + i / DSB;  // column group whose fragment part is read
-          read_frag_part<B_KC, i % DSB, MX>(bf[g], cB, wn + 16 * g, lane);
-        }
-        if constexpr (i == MI - 1) {
-          // X: this wave's reads of step kt's A fragments (issued before
-          // the RX B reads of this head) are done; once all waves are, the
-          // A stage takes step kt + 2.
-          wait_lgkmcnt<RX>();
-          __builtin_amdgcn_s_barrier();
-        }
-        if constexpr (i >= MI) {
-          constexpr int j = i - MI;  // A loads [j * BPW / AS, (j + 1) * BPW / AS)
-          static_for<j * BPW / AS, (j + 1) * BPW / AS>([&](auto J) {
-            issue_one(decltype(J)::value, kt + 2, cA, cB);
-          });
-          // MX: the A scale words of step kt + 2 after its A tile loads
-          if constexpr (i + 1 == H * MI) issue_scale_half(kt + 2, odd, false);
-        }
-      });
-      // Y: step kt + 1 has landed (its A loads went out in the previous
-      // head, its B loads in the previous tail; only this head's BPW loads,
-      // and with MX its A scale load, may be outstanding) and this wave's B
-      // reads of step kt are done.
-      wait_vmcnt<BPW + (MX ? 1 : 0)>();
-      wait_lgkmcnt<0>();
-      __builtin_amdgcn_s_barrier();
-      if (kt + 1 == KT_full && (krem & 15)) zero_tail(odd ? sA0 : sA1, odd ? sB0 : sB1);
-    };
-    auto tail = [&](auto par_tag, int kt) {
-      constexpr int P = decltype(par_tag)::value;
-      const bool odd = kt & 1;
-      uint8_t* cA = odd ? sA1 : sA0;  // this step's stage
-      uint8_t* cB = odd ? sB1 : sB0;
-      uint8_t* nA = odd ? sA0 : sA1;  // the next step's stage
-      uint8_t* nB = odd ? sB0 : sB1;
-      static_for<0, TS>([&](auto I) {
-        constexpr int i = decltype(I)::value;
-        constexpr int mi = i / (NI - H), ni = H + i % (NI - H);
-        if constexpr (MX)
-          AccTile<mi * NI + ni>::template mfma_mx<FA, FB, ni & 3, mi & 3>(
-              bf[ni], af[P][mi], sb[P][ni >> 2], sa[P][mi >> 2]);
-        else
-          AccTile<mi * NI + ni>::template mfma<FA, FB>(bf[ni], af[P][mi]);
-        // B loads [i * BPW / TS, (i + 1) * BPW / TS) of step kt + 2
-        static_for<i * BPW / TS, (i + 1) * BPW / TS>([&](auto J) {
-          issue_one(BPW + decltype(J)::value, kt + 2, cA, cB);
-        });
-        // MX: the B scale words of step kt + 2 after its B tile loads
-        if constexpr (i + 1 == TS) issue_scale_half(kt + 2, odd, true);
-        // reads [i * BP / TS, (i + 1) * BP / TS) of the next step's B fragments 0, 1
-        static_for<i * BP / TS, (i + 1) * BP / TS>([&](auto Q) {
-          constexpr int q = decltype(Q)::value;
-          read_frag_part<B_KC, q % DSB, MX>(bf[q / DSB], nB, wn + 16 * (q / DSB), lane);
-        });
-        // A reads [i * AR / TS, (i + 1) * AR / TS) of the next step, into the other buffer
-        static_for<i * (MI * DSA) / TS, (i + 1) * (MI * DSA) / TS>([&](auto Q) {
-          constexpr int q = decltype(Q)::value;
-          read_frag_part<!A_MN, q % DSA, MX>(af[P ^ 1][q / DSA], nA, wm + 16 * (q / DSA), lane);
-        });
-      });
-      if constexpr (MX) {  // the next step's scale words, into the other buffer
-        sa[P ^ 1][0] = scale_word(!odd, 0, wm / 64);
-        sa[P ^ 1][1] = scale_word(!odd, 0, wm / 64 + 1);
-        sb[P ^ 1][0] = scale_word(!odd, 1, wn / 64);
-        sb[P ^ 1][1] = scale_word(!odd, 1, wn / 64 + 1);
-      }
-    };
-
-    if (KT > 0) {
-      issue_all(0, sA0, sB0);
-      issue_scale_half(0, 0, false);
-      issue_scale_half(0, 0, true);
-      issue_all(1, sA1, sB1);
-      issue_scale_half(1, 1, false);
-      issue_scale_half(1, 1, true);
-      wait_vmcnt<LOADS_PER_STEP + (MX ? 2 : 0)>();
-      __syncthreads();
-      if (KT_full == 0 && (krem & 15)) zero_tail(sA0, sB0);
-#pragma unroll
-      for (int mi = 0; mi < MI; ++mi) af[0][mi] = read_frag<!A_MN, MX>(sA0, wm + 16 * mi, lane);
-      bf[0] = read_frag<B_KC, MX>(sB0, wn, lane);
-      bf[1] = read_frag<B_KC, MX>(sB0, wn + 16, lane);
-      if constexpr (MX) {
-        sa[0][0] = scale_word(0, 0, wm / 64);
-        sa[0][1] = scale_word(0, 0, wm / 64 + 1);
-        sb[0][0] = scale_word(0, 1, wn / 64);
-        sb[0][1] = scale_word(0, 1, wn / 64 + 1);
-      }
-      using P0 = std::integral_constant<int, 0>;
-      using P1 = std::integral_constant<int, 1>;
-      head(P0{}, 0);
-      for (int kt = 0;; kt += 2) {
-        tail(P0{}, kt);
-        if (kt + 1 >= KT) break;
-        head(P1{}, kt + 1);
-        tail(P1{}, kt + 1);
-        if (kt + 2 >= KT) break;
-        head(P0{}, kt + 2);
-      }
-      wait_vmcnt<0>();  // the (range-checked) loads of steps KT and KT + 1
-      mfma_drain();
-    }
   }
 
   // ---- epilogue: lane holds C[m][n..n+3] for each (mi, ni)
@@ -1102,45 +954,12 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
     else if (p.act == ACT_GELU_TANH) activate<ACT_GELU_TANH>(acc, e_w);
     else if (p.act == ACT_SILU) activate<ACT_SILU>(acc, e_w);
   }
-  // One wave per SIMD, intermediate epilogue, wave tile inside the matrix,
-  // no accumulator export: no per-element bounds checks, and the 16-bit
-  // encoding of two values packed with one byte permute.
-  bool stored = false;
-  if constexpr (NW == 4 && !FUSE && EPI != EPI_DIRECT) {
-    if (!p.acc_out && m0 + wm + 16 * MI <= M && n0 + wn + 16 * NI <= N) {
-      static_for<0, MI * NI>([&](auto I) {
-        constexpr int mi = decltype(I)::value / NI, ni = decltype(I)::value % NI;
-        const v4f v = AccTile<decltype(I)::value>::read();
-        lmax = fmaxf(lmax, fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))));
-        const int64_t e = (int64_t)(mb + 16 * mi) * p.ldw + nb + 16 * ni;
-        if constexpr (EPI == EPI_INTER16) {
-          // bits 16.. of u | ((u & 0xFFFF) + 0xFFFF) are sticky16(u): the
-          // added term sets bit 16 exactly when a lower bit is set
-          uint32_t x[4];
-#pragma unroll
-          for (int k = 0; k < 4; ++k) {
-            const uint32_t u = __float_as_uint(v[k]);
-            x[k] = u | ((u & 0xFFFFu) + 0xFFFFu);
-          }
-          *(v2i*)((uint16_t*)p.inter + e) =
-              v2i{(int)__builtin_amdgcn_perm(x[1], x[0], 0x07060302u),
-                  (int)__builtin_amdgcn_perm(x[3], x[2], 0x07060302u)};
-        } else {
-          *(v4f*)((float*)p.inter + e) = v;
-        }
-      });
-      stored = true;
-    }
-  }
-  if (!stored) static_for<0, MI * NI>([&](auto I) {
+  static_for<0, MI * NI>([&](auto I) {
     constexpr int mi = decltype(I)::value / NI, ni = decltype(I)::value % NI;
     const int m = mb + 16 * mi;
     const int n = nb + 16 * ni;
     if (m < M && n < N) {
-      // FUSE: w; one wave per SIMD: read from the tile's AGPRs
-      v4f v;
-      if constexpr (NW == 4) v = AccTile<decltype(I)::value>::read();
-      else v = acc[mi][ni];
+      const v4f v = acc[mi][ni];  // FUSE: w
       lmax = fmaxf(lmax, fabsf(v[0]));
       if (n + 1 < N) lmax = fmaxf(lmax, fabsf(v[1]));
       if (n + 2 < N) lmax = fmaxf(lmax, fabsf(v[2]));
@@ -1224,86 +1043,6 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmParams p) {
     for (int w = 1; w < WAVES; ++w) wmax = fmaxf(wmax, red[w]);
     atomicMax(p.hdr, __float_as_uint(wmax));
   }
-}
-
-// Launch of one (layout, fused or not) family over the format pairs and
-// epilogues; each family is instantiated in a source file of its own
-// (gemm_<layout>[_fused].hip) so that they compile in parallel.
-template <bool A_MN, bool B_KC, bool FUSE>
-hipError_t launch_layout(const GemmParams& p, int fa, int fb, int epi, hipStream_t s);
-
-// Wave arrangement per kernel: one wave per SIMD where the epilogue stores
-// the pre-cast intermediate (its main loop is the faster one); two waves
-// per SIMD where the epilogue converts every value itself (direct cast of
-// the delayed rescale, fused add / activation), whose arithmetic the second
-// wave of a SIMD overlaps with the first one's stores.
-constexpr int gemm_waves(int epi, bool fuse) { return (fuse || epi == EPI_DIRECT) ? 8 : 4; }
-
-template <bool A_MN, bool B_KC, bool FUSE, int FA, int FB, int EPI>
-hipError_t launch_epi(const GemmParams& p, hipStream_t s) {
-  constexpr int NW = gemm_waves(EPI, FUSE);
-  const dim3 grid(p.tiles_m * p.tiles_n), block(WaveCfg<NW>::NTHR);
-  if constexpr (FUSE) {
-    if (p.ch_a || p.ch_b) {
-      hipLaunchKernelGGL((gemm_kernel<A_MN, B_KC, FA, FB, EPI, FUSE, NW, true>), grid, block, 0, s, p);
-      return hipGetLastError();
-    }
-  }
-  hipLaunchKernelGGL((gemm_kernel<A_MN, B_KC, FA, FB, EPI, FUSE, NW>), grid, block, 0, s, p);
-  return hipGetLastError();
-}
-
-template <bool A_MN, bool B_KC, bool FUSE, int FA, int FB>
-hipError_t launch_fmt(const GemmParams& p, int epi, hipStream_t s) {
-  switch (epi) {
-    case EPI_INTER16:
-      return launch_epi<A_MN, B_KC, FUSE, FA, FB, EPI_INTER16>(p, s);
-    case EPI_INTER32:
-      return launch_epi<A_MN, B_KC, FUSE, FA, FB, EPI_INTER32>(p, s);
-    default:
-      return launch_epi<A_MN, B_KC, FUSE, FA, FB, EPI_DIRECT>(p, s);
-  }
-}
-
-// MX block scales: the 4-wave kernel with the fp32 intermediate (NONE,
-// AMAX), the 8-wave kernel with the direct cast (DELAYED) and for A and B
-// both stored k-major (A [K][M], B [K][N]), whose 4-wave variant does not
-// fit its registers (the build check rejects its spills); one source file
-// per layout (gemm_<layout>_mx.hip).
-constexpr int mx_waves(bool a_mn, bool b_kc, int epi) {
-  return (epi == EPI_DIRECT || (a_mn && !b_kc)) ? 8 : 4;
-}
-template <bool A_MN, bool B_KC>
-hipError_t launch_layout_mx(const GemmParams& p, int fa, int fb, int epi, hipStream_t s);
-
-template <bool A_MN, bool B_KC, int FA, int FB>
-hipError_t launch_mx(const GemmParams& p, int epi, hipStream_t s) {
-  const dim3 grid(p.tiles_m * p.tiles_n);
-  if (epi == EPI_DIRECT)
-    hipLaunchKernelGGL((gemm_kernel<A_MN, B_KC, FA, FB, EPI_DIRECT, false, 8, false, true>), grid,
-                       dim3(WaveCfg<8>::NTHR), 0, s, p);
-  else
-    hipLaunchKernelGGL(
-        (gemm_kernel<A_MN, B_KC, FA, FB, EPI_INTER32, false, mx_waves(A_MN, B_KC, EPI_INTER32), false,
-                     true>),
-        grid, dim3(WaveCfg<mx_waves(A_MN, B_KC, EPI_INTER32)>::NTHR), 0, s, p);
-  return hipGetLastError();
-}
-
-template <bool A_MN, bool B_KC>
-hipError_t launch_formats_mx(const GemmParams& p, int fa, int fb, int epi, hipStream_t s) {
-  if (fa == kE4M3 && fb == kE4M3) return launch_mx<A_MN, B_KC, kE4M3, kE4M3>(p, epi, s);
-  if (fa == kE4M3 && fb == kE5M2) return launch_mx<A_MN, B_KC, kE4M3, kE5M2>(p, epi, s);
-  if (fa == kE5M2 && fb == kE4M3) return launch_mx<A_MN, B_KC, kE5M2, kE4M3>(p, epi, s);
-  return launch_mx<A_MN, B_KC, kE5M2, kE5M2>(p, epi, s);
-}
-
-template <bool A_MN, bool B_KC, bool FUSE>
-hipError_t launch_formats(const GemmParams& p, int fa, int fb, int epi, hipStream_t s) {
-  if (fa == kE4M3 && fb == kE4M3) return launch_fmt<A_MN, B_KC, FUSE, kE4M3, kE4M3>(p, epi, s);
-  if (fa == kE4M3 && fb == kE5M2) return launch_fmt<A_MN, B_KC, FUSE, kE4M3, kE5M2>(p, epi, s);
-  if (fa == kE5M2 && fb == kE4M3) return launch_fmt<A_MN, B_KC, FUSE, kE5M2, kE4M3>(p, epi, s);
-  return launch_fmt<A_MN, B_KC, FUSE, kE5M2, kE5M2>(p, epi, s);
 }
 
 }  // namespace scalify

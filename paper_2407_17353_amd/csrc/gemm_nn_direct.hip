@@ -1,0 +1,13 @@
+// Instantiations of the scaled FP8 GEMM with the direct cast (output scale known before the
+// GEMM: delayed or no rescale) for
+// A stored [M][K] and B stored [K][N].
+#include "gemm4_kernel.h"
+
+namespace scalify {
+
+template <>
+hipError_t launch_layout_direct<false, false>(const GemmParams& p, int fa, int fb, int, hipStream_t s) {
+  return by_formats<DirectFamily<false, false, false>::template F>(p, fa, fb, s);
+}
+
+}  // namespace scalify

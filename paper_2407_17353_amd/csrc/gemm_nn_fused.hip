@@ -1,13 +1,13 @@
-// Instantiations of the scaled FP8 GEMM with the fused residual add and
-// activation epilogue, for A stored [M][K] and B stored [K][N].
-#include "gemm_kernel.h"
+// Instantiations of the scaled FP8 GEMM with the fused residual add, activation and channel
+// scales for
+// A stored [M][K] and B stored [K][N].
+#include "gemm4_kernel.h"
 
 namespace scalify {
 
 template <>
-hipError_t launch_layout<false, false, true>(const GemmParams& p, int fa, int fb, int epi,
-                                                 hipStream_t s) {
-  return launch_formats<false, false, true>(p, fa, fb, epi, s);
+hipError_t launch_layout<false, false, true>(const GemmParams& p, int fa, int fb, int, hipStream_t s) {
+  return by_formats<PlainFamily<false, false, true>::template F>(p, fa, fb, s);
 }
 
 }  // namespace scalify

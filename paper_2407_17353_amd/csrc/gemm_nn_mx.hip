@@ -1,13 +1,12 @@
-// Instantiations of the scaled FP8 GEMM with MX block scales for A stored
-// [M][K] and B stored [K][N].
-#include "gemm_kernel.h"
+// Instantiations of the scaled FP8 GEMM with MX block scales and the direct cast for
+// A stored [M][K] and B stored [K][N].
+#include "gemm4_kernel.h"
 
 namespace scalify {
 
 template <>
-hipError_t launch_layout_mx<false, false>(const GemmParams& p, int fa, int fb, int epi,
-                                        hipStream_t s) {
-  return launch_formats_mx<false, false>(p, fa, fb, epi, s);
+hipError_t launch_layout_mx<false, false>(const GemmParams& p, int fa, int fb, int, hipStream_t s) {
+  return by_formats<DirectFamily<false, false, true>::template F>(p, fa, fb, s);
 }
 
 }  // namespace scalify

@@ -11,9 +11,12 @@ namespace scalify {
 //       the input scales, or the scaled-add exponent with a residual):
 //       snapshot taken by the prologue, so that an output scale aliasing an
 //       input scale cannot race
-//   [2] delayed rescale: the shift of the direct cast, data' = w * 2^-shift
+//   [2] direct cast (delayed rescale, or none): its shift, data' = w * 2^-shift
 //   [3] fused residual add: shift of acc into w's scale (e_a + e_b - e_w)
 //   [4] fused residual add: shift of the residual (q - e_w)
+//   [5] single pass: workgroups arrived at the grid barrier (zeroed by the prologue)
+//   [6] single pass: barrier state, 0 running, 1 complete, 2 aborted (zeroed by the prologue)
+//   [7] single pass: workgroups that wrote their held tile after an abort (zeroed by the prologue)
 constexpr size_t kHeaderBytes = 256;
 
 // Activation of the fused epilogue (values of scalify_activation).
@@ -62,7 +65,24 @@ struct GemmParams {
   const uint8_t* mx_b;
   int mx_groups_a, mx_groups_b;
   uint32_t mx_a_bytes, mx_b_bytes;
+  // The persistent 4-wave kernel: workgroups (gemm4_grid), and the single
+  // pass of the dynamic rescale (EPI_INTER16 / EPI_INTER32 kernels that hold
+  // their last tile, meet at a grid barrier and cast): its rescale target,
+  // the output scale and statistic it writes, and the barrier's wait budget
+  // in ticks of the 100 MHz real-time counter.
+  int grid;
+  int epi;  // Epi of the launch (set by launch_gemm)
+  int single_pass;
+  int target;
+  float* out_scale;
+  float* amax_out;
+  int64_t spin_ticks;
 };
+
+// Workgroups of the persistent 4-wave kernel for `tiles` output tiles: one
+// per CU of the current device (its LDS holds one workgroup), at most one
+// per tile.
+int gemm4_grid(int tiles);
 
 // Packed MX block scales (see GemmParams) from row-major bytes src[r * ld + b].
 hipError_t launch_mx_pack(const uint8_t* src, int rows, int K, int ld, uint8_t* dst,
@@ -76,21 +96,23 @@ hipError_t launch_gemm(const GemmParams& p, bool a_mn, bool b_kc, int fa, int fb
 // Prologue: hdr[0] = 0, hdr[1] = exponent(s0) + exponent(s1) (NULL = scale 1).
 hipError_t launch_prologue(uint32_t* hdr, const float* s0, const float* s1, hipStream_t s);
 
-// Prologue of the matmul: hdr[0] = 0 and hdr[1] = e_w, the scale exponent of
-// the pre-cast value: e_a + e_b, or with a residual of scale 2^q the scaled
-// add exponent max(e_a + e_b + e_c, q) (sqrt(s_p^2 + s_r^2) rounded down),
-// with hdr[3] = e_a + e_b - e_w and hdr[4] = q - e_w. Delayed rescale: the
-// output scale from the statistic *amax_in of an earlier call (e_r =
-// floor(log2 amax_in) - target, 0 when amax_in is 0, Inf or NaN): writes
-// *out_scale = 2^e_out, e_out = clamp(e_w + e_cc + e_r), and hdr[2] =
-// e_out - e_w, where e_cc = e_c without a residual and 0 with one.
+// Prologue of the matmul: hdr[0] = hdr[5] = hdr[6] = hdr[7] = 0 and hdr[1] =
+// e_w, the scale exponent of the pre-cast value: e_a + e_b, or with a
+// residual of scale 2^q the scaled add exponent max(e_a + e_b + e_c, q)
+// (sqrt(s_p^2 + s_r^2) rounded down), with hdr[3] = e_a + e_b - e_w and
+// hdr[4] = q - e_w. Direct cast (output scale known before the GEMM): from
+// the statistic *amax_in of an earlier call (delayed rescale; e_r =
+// floor(log2 amax_in) - target, 0 when amax_in is 0, Inf or NaN) or with
+// e_r = 0 (no rescale, amax_in NULL): writes *out_scale = 2^e_out, e_out =
+// clamp(e_w + e_cc + e_r), and hdr[2] = e_out - e_w, where e_cc = e_c
+// without a residual and 0 with one.
 struct MatmulPrologue {
   const float* s0;
   const float* s1;
   const float* s_res;  // residual scale (NULL = 1)
   int residual;        // 1: scaled add of a residual
   int e_c;
-  int delayed;
+  int direct;
   const float* amax_in;
   int target;
   float* out_scale;

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <stdlib.h>
+
 #include <mutex>
 
 #include "../../include/scalify.h"
@@ -44,9 +46,44 @@ size_t matmul_ws(int64_t M, int64_t N, int32_t out_dtype, int32_t rescale, bool 
   if (M < 0 || N < 0 || !is_out(out_dtype) || rescale < SCALIFY_RESCALE_NONE ||
       rescale > SCALIFY_RESCALE_DELAYED)
     return 0;
-  if (rescale == SCALIFY_RESCALE_DELAYED) return kHeaderBytes;  // codes written by the GEMM
+  // DELAYED and NONE: codes written by the GEMM (the output scale is known
+  // before it runs)
+  if (rescale != SCALIFY_RESCALE_AMAX) return kHeaderBytes;
   const size_t bytes = (out_dtype == SCALIFY_F16 || fused) ? 4u : 2u;
   return kHeaderBytes + (size_t)M * (size_t)round_up(N, 16) * bytes;
+}
+
+// The single pass of the dynamic rescale (GEMM, grid barrier on the
+// statistic, cast: one kernel) where every workgroup of the persistent grid
+// holds one tile (no intermediate at all: it is faster there), the GEMM +
+// cast kernel pair otherwise (the earlier tiles' intermediate, cast by the
+// 4 waves of a CU after the barrier, is slower than the cast kernel).
+// SCALIFY_SINGLE_PASS=1 takes the single pass wherever it can run, 0 never.
+bool single_pass_choice(int64_t tiles, int grid) {
+  const char* v = getenv("SCALIFY_SINGLE_PASS");
+  if (v && v[0] == '1' && v[1] == 0) return true;
+  if (v && v[0] == '0' && v[1] == 0) return false;
+  return tiles <= grid;
+}
+
+// The 4-wave kernel is persistent (one workgroup per CU walks its tiles)
+// unless SCALIFY_PERSISTENT=0, which launches one workgroup per tile (and
+// then no single pass, whose barrier needs the grid co-resident).
+bool persistent_enabled() {
+  const char* v = getenv("SCALIFY_PERSISTENT");
+  return !(v && v[0] == '0' && v[1] == 0);
+}
+
+// Wait budget of the single pass's grid barrier, in ticks of the 100 MHz
+// real-time counter: far beyond the arrival skew of a co-resident grid (at
+// most one tile's main loop, about a microsecond per 128-deep k-step, plus
+// its epilogue): 20 ms + 4 us per k-step. SCALIFY_SPIN_TICKS overrides it
+// (0: a workgroup that is not the last to arrive gives up at once, which
+// exercises the recovery of a grid that is not co-resident).
+int64_t spin_ticks(int64_t K) {
+  const char* v = getenv("SCALIFY_SPIN_TICKS");
+  if (v && v[0]) return strtoll(v, nullptr, 10);
+  return 2000000 + 400 * ((K + 127) / 128);
 }
 
 bool is_fused(const scalify_matmul_opts* o) {
@@ -269,15 +306,24 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
   const int e_c = scalify_matmul_scale_log2(K);
   const bool amax_mode = opts->rescale == SCALIFY_RESCALE_AMAX;
   const bool delayed = opts->rescale == SCALIFY_RESCALE_DELAYED;
-  // Delayed: the output scale comes from the statistic of an earlier call,
-  // so the GEMM casts straight to codes (no intermediate). Otherwise the GEMM
-  // writes a pre-cast intermediate: 16-bit for FP8 outputs of the plain
-  // epilogue, fp32 for FP16 outputs, for fused epilogues and with block
-  // scales (whose accumulators may be fp32 subnormals, which the 16-bit
-  // encoding does not keep exactly).
-  const int epi = delayed ? EPI_DIRECT
-                          : ((opts->out_dtype == SCALIFY_F16 || fused || mx) ? EPI_INTER32
-                                                                              : EPI_INTER16);
+  // Delayed or no rescale: the output scale is known before the GEMM runs
+  // (from the statistic of an earlier call, or the propagated scale itself),
+  // so the GEMM casts straight to codes (no intermediate). Dynamic rescale:
+  // the GEMM writes a pre-cast intermediate: 16-bit for FP8 outputs of the
+  // plain epilogue, fp32 for FP16 outputs, for fused epilogues and with
+  // block scales (whose accumulators may be fp32 subnormals, which the
+  // 16-bit encoding does not keep exactly); the single pass keeps each
+  // workgroup's last tile out of it and casts in the same kernel.
+  const int epi = !amax_mode ? EPI_DIRECT
+                             : ((opts->out_dtype == SCALIFY_F16 || fused || mx) ? EPI_INTER32
+                                                                                 : EPI_INTER16);
+  const bool tn_mx = mx && a->trans != 0 && b->trans == 0;  // 8-wave kernel
+  // (the 4-wave block-scaled kernel casts only in the single pass)
+  const bool persistent = persistent_enabled();
+  const int64_t tiles = ((M + 255) / 256) * ((N + 255) / 256);
+  const int grid = persistent ? gemm4_grid((int)tiles) : (int)tiles;
+  const bool single_pass =
+      amax_mode && !fused && !tn_mx && persistent && single_pass_choice(tiles, grid);
   // Exponent offset of the statistic: the matmul data is acc * 2^-e_c; with
   // a residual the statistic is taken over w itself.
   const int e_cc = res ? 0 : e_c;
@@ -288,8 +334,8 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
   pq.s_res = res ? res->scale : nullptr;
   pq.residual = res ? 1 : 0;
   pq.e_c = e_c;
-  pq.delayed = delayed ? 1 : 0;
-  pq.amax_in = opts->amax_in;
+  pq.direct = epi == EPI_DIRECT ? 1 : 0;
+  pq.amax_in = delayed ? opts->amax_in : nullptr;
   pq.target = opts->target_log2;
   pq.out_scale = out->scale;
   if (launch_matmul_prologue(hdr, pq, s) != hipSuccess) return SCALIFY_ERR_HIP;
@@ -329,6 +375,12 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
   p.mx_groups_b = (int)((N + 63) / 64);
   p.mx_a_bytes = (uint32_t)mx_a_bytes;
   p.mx_b_bytes = (uint32_t)mx_b_bytes;
+  p.grid = grid;
+  p.single_pass = single_pass ? 1 : 0;
+  p.target = opts->target_log2;
+  p.out_scale = out->scale;
+  p.amax_out = opts->amax_out;
+  p.spin_ticks = spin_ticks(K);
   hipEvent_t* ev = (hipEvent_t*)opts->events;
   if (ev && ev[0] && hipEventRecord(ev[0], s) != hipSuccess) return SCALIFY_ERR_HIP;
   if (M > 0 && N > 0) {
@@ -337,13 +389,29 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
       return SCALIFY_ERR_HIP;
   }
   if (ev && ev[1] && hipEventRecord(ev[1], s) != hipSuccess) return SCALIFY_ERR_HIP;
-  if (delayed) {
-    // The statistic this call records for the next one.
+  if (epi == EPI_DIRECT) {
+    // The statistic this call records (for the next one, when delayed).
     if (opts->amax_out && launch_finalize_amax(hdr, e_cc, opts->amax_out, s) != hipSuccess)
       return SCALIFY_ERR_HIP;
+  } else if (single_pass) {
+    // The GEMM has cast the output and written its scale and statistic; with
+    // nothing to compute (an empty output) they are written here.
+    if (M == 0 || N == 0) {
+      EpilogueParams q = {};
+      q.M = 0;
+      q.N = (int)N;
+      q.e_c = e_cc;
+      q.target = opts->target_log2;
+      q.mode = 1;
+      q.hdr = hdr;
+      q.out_scale = out->scale;
+      q.amax_out = opts->amax_out;
+      if (launch_epilogue_cast(q, epi == EPI_INTER32, opts->out_dtype, s) != hipSuccess)
+        return SCALIFY_ERR_HIP;
+    }
   } else {
-    // Second pass: global amax -> rescale exponent -> output scale, and the
-    // cast of the intermediate (also for NONE mode, where e_r = 0).
+    // Second pass of the two-kernel dynamic rescale: global amax -> rescale
+    // exponent -> output scale, and the cast of the intermediate.
     EpilogueParams q = {};
     q.inter = p.inter;
     q.ldw = p.ldw;
@@ -354,7 +422,7 @@ scalify_status scalify_matmul(const scalify_scaled_array* a, const scalify_scale
     q.e_c = e_cc;
     q.target = opts->target_log2;
     q.sat = p.sat;
-    q.mode = amax_mode ? 1 : 0;
+    q.mode = 1;
     q.hdr = hdr;
     q.out_scale = out->scale;
     q.amax_out = opts->amax_out;
