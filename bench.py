@@ -34,7 +34,8 @@ PEAK_FP8_TFLOPS = 5000.0      # MI355X dense FP8 MFMA, 256 CU x 2.4 GHz x 8192 F
 PEAK_HBM_GBS = 8000.0
 EVENT_EVERY = 4               # GEMM-bracketing events on every 4th timed call
 FMT_NAME = {0: "e4m3", 1: "e5m2", 2: "f16"}
-GEMM_SOURCES = ("paper_2407_17353_amd/csrc/gemm_kernel.h", "paper_2407_17353_amd/csrc/gemm_nn.hip",
+GEMM_SOURCES = ("paper_2407_17353_amd/csrc/gemm4_kernel.h", "paper_2407_17353_amd/csrc/gemm_kernel.h",
+                "paper_2407_17353_amd/csrc/gemm_nn.hip", "paper_2407_17353_amd/csrc/ew_util.h",
                 "paper_2407_17353_amd/csrc/codec.h", "paper_2407_17353_amd/csrc/kernels.h")
 TRAFFIC_SUMMARY = "profiles/gemm_8192cube_e4m3_hbm_traffic.md"
 
