@@ -83,6 +83,34 @@ __device__ __forceinline__ v2i cast4_f16_any(const v4f& v, bool fast, float inv,
   return v2i{(int)(c[0] | (c[1] << 16)), (int)(c[2] | (c[3] << 16))};
 }
 
+// Running max of |a|, |b| and m (m >= 0), one instruction: the fast
+// epilogues call it on values known not to be NaN.
+__device__ __forceinline__ float max3_abs(float m, float a, float b) {
+  float r;
+  asm("v_max3_f32 %0, %1, |%2|, |%3|" : "=v"(r) : "v"(m), "v"(a), "v"(b));
+  return r;
+}
+
+// 4 non-NaN fp32 values times inv = 2^-shift (inside the fast window) to
+// FP16, two codes per word: the product is exact unless it leaves the fp32
+// normal range (above it the conversion overflows as the exact value would,
+// below it the value rounds to zero in FP16 either way; the product keeps
+// the sign of a zero), converted with round to nearest even. SAT clamps the
+// product to +-65504 first, which is what saturation gives for every value
+// that would overflow.
+template <bool SAT>
+__device__ __forceinline__ v2i cvt4_f16_fast(float x0, float x1, float x2, float x3, float inv) {
+  float y[4] = {x0 * inv, x1 * inv, x2 * inv, x3 * inv};
+  if constexpr (SAT) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) y[i] = __builtin_amdgcn_fmed3f(y[i], -65504.0f, 65504.0f);
+  }
+  int lo, hi;
+  asm("v_cvt_pk_f16_f32 %0, %1, %2" : "=v"(lo) : "v"(y[0]), "v"(y[1]));
+  asm("v_cvt_pk_f16_f32 %0, %1, %2" : "=v"(hi) : "v"(y[2]), "v"(y[3]));
+  return v2i{lo, hi};
+}
+
 // The cast kernel's arithmetic on one 16-element chunk of the intermediate
 // (fp32 bits, or 16-bit encodings shifted into the top half), call-free.
 template <int OUTF>
@@ -399,7 +427,61 @@ __global__ __launch_bounds__(256, 1) void gemm4_kernel(GemmParams p) {
         *(v4f*)((float*)p.inter + (int64_t)m * p.ldw + n) = v;  // (ldw: 16 elements)
       }
     };
-    if (!p.acc_out && m0 + wm + 16 * MI <= M && n0 + wn + 16 * NI <= N) {
+    const bool inside = !p.acc_out && m0 + wm + 16 * MI <= M && n0 + wn + 16 * NI <= N;
+    if constexpr (OUTF >= 0) {
+      // Codes of a wave tile inside the matrix with the shift inside the fast
+      // window: the conversion scales by itself, saturation is chosen once
+      // for the tile, and a group holding a NaN (rare) takes a branch that
+      // puts the NaN codes in and keeps the NaN out of the statistic.
+      auto codes = [&](auto sat_tag) {
+        constexpr bool SAT = decltype(sat_tag)::value;
+        static_for<0, MI * NI>([&](auto I) {
+          constexpr int t = decltype(I)::value;
+          constexpr int mi = t / NI, ni = t % NI;
+          const v4f v = AccTile<t>::read();
+          if constexpr (ZERO) AccTile<t>::zero();
+          float x[4] = {v[0], v[1], v[2], v[3]};
+          const int64_t e = (int64_t)(mb + 16 * mi) * p.ldc + nb + 16 * ni;
+          if constexpr (OUTF == kF16) {
+            v2i w = cvt4_f16_fast<SAT>(x[0], x[1], x[2], x[3], inv);
+            if (__builtin_expect(x[0] != x[0] || x[1] != x[1] || x[2] != x[2] || x[3] != x[3], 0)) {
+              uint32_t h[4] = {(uint32_t)w.x & 0xFFFFu, (uint32_t)w.x >> 16, (uint32_t)w.y & 0xFFFFu,
+                               (uint32_t)w.y >> 16};
+#pragma unroll
+              for (int i = 0; i < 4; ++i)
+                if (x[i] != x[i]) {
+                  h[i] = FmtTraits<kF16>::NANC | ((__float_as_uint(x[i]) >> 16) & 0x8000u);
+                  x[i] = 0.f;
+                }
+              w = v2i{(int)(h[0] | (h[1] << 16)), (int)(h[2] | (h[3] << 16))};
+            }
+            *(v2i*)((uint16_t*)p.out + e) = w;
+          } else {
+            uint32_t w = cast4_fp8_hw<OUTF>(__float_as_uint(x[0]), __float_as_uint(x[1]),
+                                            __float_as_uint(x[2]), __float_as_uint(x[3]), scale, SAT);
+            if (__builtin_expect(x[0] != x[0] || x[1] != x[1] || x[2] != x[2] || x[3] != x[3], 0)) {
+#pragma unroll
+              for (int i = 0; i < 4; ++i)
+                if (x[i] != x[i]) {
+                  const uint32_t c = FmtTraits<OUTF>::NANC | ((__float_as_uint(x[i]) >> 24) & 0x80u);
+                  w = (w & ~(0xFFu << (8 * i))) | (c << (8 * i));
+                  x[i] = 0.f;
+                }
+            }
+            *(uint32_t*)((uint8_t*)p.out + e) = w;
+          }
+          lmax = max3_abs(max3_abs(lmax, x[0], x[1]), x[2], x[3]);
+        });
+      };
+      if (inside && fast) {
+        if (sat)
+          codes(std::true_type{});
+        else
+          codes(std::false_type{});
+        return;
+      }
+    }
+    if (inside) {
       // wave tile inside the matrix: no per-element checks
       static_for<0, MI * NI>([&](auto I) {
         constexpr int t = decltype(I)::value;
