@@ -279,10 +279,72 @@ def cpu_baseline(case, target_s):
         m = int(min(case.M, max(m, m * target_s / max(t, 1e-3))) // threads * threads) or threads
         t = run(m)
     flops = 2.0 * m * case.N * case.K
-    return {"value": flops / t / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
-            "sample": f"rows 0..{m - 1} of A (a {m}x{case.N}x{case.K} scaled matmul: fp64 "
-                      f"accumulation, amax rescale and cast), {t:.1f} s",
-            "seconds": round(t, 2), "rows": m}
+    res = {"value": flops / t / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+           "sample": f"rows 0..{m - 1} of A (a {m}x{case.N}x{case.K} scaled matmul: fp64 "
+                     f"accumulation, amax rescale and cast), {t:.1f} s",
+           "seconds": round(t, 2), "rows": m, "cpu_model": cpu_model()}
+    res["per_config"] = oracle_per_config(threads)
+    res["config1_one_core"] = oracle_config1_one_core()
+    return res
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _oracle_sample(case, m):
+    """Seconds of the oracle on logical rows 0..m-1 of A of one GemmCase."""
+    from oracle import oracle as orc
+    A = case.make_a("cpu").numpy()
+    B = case.make_b("cpu").numpy()
+    Asub = A[:, :m].copy() if case.ta else A[:m]
+    t = time.perf_counter()
+    orc.matmul(Asub, case.fa, case.ta, 2.0 ** case.a_scale_log2, B, case.fb, case.tb,
+               2.0 ** case.b_scale_log2, out_fmt=case.fout)
+    return time.perf_counter() - t
+
+
+def oracle_per_config(threads, budget_s=1.5):
+    """The oracle on the first GEMM of every configuration: a row sample
+    sized for about budget_s seconds, its rate, and the whole GEMM's time
+    extrapolated from it (the oracle's time is linear in the rows)."""
+    from paper_2407_17353_amd import workloads as wl
+    out = {}
+    for cfg, cases in wl.all_configs().items():
+        c = cases[0]
+        m = min(c.M, max(1, threads))
+        t = _oracle_sample(c, m)
+        if t < budget_s / 4 and m < c.M:
+            m = min(c.M, int(m * budget_s / max(t, 1e-3)))
+            t = _oracle_sample(c, m)
+        rate = 2.0 * m * c.N * c.K / t
+        out[f"config{cfg}"] = {"gemm": c.name, "M": c.M, "N": c.N, "K": c.K, "rows": m,
+                               "seconds": round(t, 3), "tflops": round(rate / 1e12, 5),
+                               "whole_gemm_s_est": round(c.flops / rate, 4)}
+    return out
+
+
+def oracle_config1_one_core():
+    """Configuration 1 (256^3) in full on one thread of the CPU."""
+    import ctypes
+    from paper_2407_17353_amd import workloads as wl
+    c = wl.config_1()[0]
+    gomp = ctypes.CDLL("libgomp.so.1")
+    n0 = gomp.omp_get_max_threads()
+    gomp.omp_set_num_threads(1)
+    try:
+        t = _oracle_sample(c, c.M)
+    finally:
+        gomp.omp_set_num_threads(n0)
+    return {"gemm": c.name, "seconds": round(t, 4), "tflops": round(c.flops / t / 1e12, 6),
+            "cores": 1}
 
 
 def main():

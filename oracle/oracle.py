@@ -34,7 +34,9 @@ ACT_NONE, ACT_RELU, ACT_GELU_TANH, ACT_SILU = 0, 1, 2, 3
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "scalify_oracle.c")
-_LIB = os.path.join(_HERE, "liboracle.so")
+# SCALIFY_ORACLE_LIB names another build of the same source (e.g. one with
+# the address and undefined-behaviour sanitizers) to load instead.
+_LIB = os.environ.get("SCALIFY_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 
 _lib = None
 
