@@ -161,6 +161,123 @@ __global__ __launch_bounds__(LN_THREADS) void ln_fwd_kernel(LnParams p) {
   }
 }
 
+// The forward for rows of 2049 .. 4096 FP16 or FP8 elements, each row
+// crossing HBM once: a wave holds its row's raw codes in registers (lane l
+// the 16-element chunks l + 64 j, j < 4) and loads the next row of its
+// stride while it computes this one (two buffers); gamma and beta sit in LDS
+// for the workgroup's rows. The statistics and the output are computed in the
+// order ln_row_stats and ln_fwd_kernel use, so the two kernels give the same
+// bits. FULL: D = 4096, every chunk of every lane whole (no checks).
+constexpr int LN_PIPE_NJ = 4;
+constexpr int LN_PIPE_D = 1024 * LN_PIPE_NJ;
+
+template <int XF>
+__device__ __forceinline__ float ln_raw_decode(const uint32_t* w, int i) {
+  if constexpr (XF == kF16) return decode_hw<kF16>((w[i >> 1] >> (16 * (i & 1))) & 0xFFFFu);
+  else return decode_hw<XF>((w[i >> 2] >> (8 * (i & 3))) & 0xFFu);
+}
+
+template <int XF, int OUTF, bool FULL>
+__global__ __launch_bounds__(LN_THREADS) void ln_fwd_pipe_kernel(LnParams p) {
+  constexpr int NJ = LN_PIPE_NJ;
+  constexpr int WPC = XF == kF16 ? 8 : 4;  // dwords per 16-element chunk
+  __shared__ __attribute__((aligned(16))) float s_g[LN_PIPE_D];
+  __shared__ __attribute__((aligned(16))) float s_b[LN_PIPE_D];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const bool sat = p.sat != 0;
+  const int D = p.D;
+  const int nch = (D + 15) / 16;
+  for (int e = threadIdx.x; e < 16 * nch; e += LN_THREADS) {
+    s_g[e] = (p.gamma && e < D) ? p.gamma[e] : 1.0f;
+    s_b[e] = (p.beta && e < D) ? p.beta[e] : 0.0f;
+  }
+  __syncthreads();
+  if (blockIdx.x == 0 && threadIdx.x == 0) *p.out_scale = 1.0f;  // Appendix C.2: scale 1
+  const int64_t stride = (int64_t)gridDim.x * 4;
+  // raw codes of row r (zeros past D and for r >= R)
+  auto load_row = [&](int64_t r, uint32_t (&w)[NJ][WPC]) {
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int q = lane + 64 * j;
+      const int valid = D - 16 * q;
+#pragma unroll
+      for (int k = 0; k < WPC; ++k) w[j][k] = 0u;
+      if (r < p.R && (FULL || q < nch)) {
+        const int64_t e = r * p.ldx + 16 * q;
+        if (FULL || valid >= 16) {
+#pragma unroll
+          for (int h = 0; h < WPC / 4; ++h) {
+            const u4 v = XF == kF16 ? *((const u4*)((const uint16_t*)p.x + e) + h)
+                                    : *((const u4*)((const uint8_t*)p.x + e) + h);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) w[j][4 * h + k] = v[k];
+          }
+        } else {
+          constexpr int EPW = XF == kF16 ? 2 : 4;  // elements per dword
+#pragma unroll
+          for (int i = 0; i < 16; ++i)
+            if (i < valid) w[j][i / EPW] |= load1<XF>(p.x, e + i) << ((32 / EPW) * (i % EPW));
+        }
+      }
+    }
+  };
+  auto process = [&](int64_t r, const uint32_t (&w)[NJ][WPC]) {
+    float s = 0.0f;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      if (FULL || lane + 64 * j < nch) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) s += ln_raw_decode<XF>(w[j], i);  // columns >= D are 0
+      }
+    const float mu = wave_sum(s) / (float)D;
+    float t = 0.0f;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int q = lane + 64 * j;
+      if (FULL || q < nch) {
+        const int valid = FULL ? 16 : D - 16 * q;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const float d = ln_raw_decode<XF>(w[j], i) - mu;
+          t += i < valid ? d * d : 0.0f;
+        }
+      }
+    }
+    const float sigma = sqrtf(wave_sum(t) / (float)D);
+    const float inv = 1.0f / (sigma + p.eps);
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int q = lane + 64 * j;
+      if (FULL || q < nch) {
+        const int n = 16 * q;
+        const int valid = FULL ? 16 : D - n;
+        float y[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          y[i] = (ln_raw_decode<XF>(w[j], i) - mu) * inv * s_g[n + i] + s_b[n + i];
+        if (p.pre_out) ln_store_f32(p.pre_out + r * (int64_t)D + n, valid, y);
+        ln_store16<OUTF>(p.out, r * p.ldo + n, valid, y, 0, 1.0f, true, sat);
+      }
+      // one chunk's gamma, beta and outputs at a time: bounded registers
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  uint32_t wa[NJ][WPC], wb[NJ][WPC];
+  int64_t r = (int64_t)blockIdx.x * 4 + wave;
+  load_row(r, wa);
+#pragma unroll 1
+  while (r < p.R) {
+    load_row(r + stride, wb);
+    process(r, wa);
+    r += stride;
+    if (r >= p.R) break;
+    load_row(r + stride, wa);
+    process(r, wb);
+    r += stride;
+  }
+}
+
 // Per-row numbers of the gradient (rowstats[r] = {mean, 1/(std+eps), mean(g),
 // mean(g * xhat)/std or 0}), so that dx = (dy gamma - mean(g) - (x - mean) t) * inv.
 // Both backward kernels evaluate it with this code and no contraction, so the
@@ -331,9 +448,41 @@ int64_t layernorm_ws_floats(int64_t R, int64_t D) {
   return 4 * R + layernorm_row_tiles(R) * 2 * layernorm_param_stride(D);
 }
 
+// Workgroups of the pipelined forward: three per CU, each wave walking rows
+// with the grid's stride.
+static int pipe_grid(int64_t R) {
+  static int cus = 0;  // (a benign race: every thread computes the same value)
+  if (cus <= 0) {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    cus = n;
+  }
+  const int64_t need = (R + 3) / 4;
+  const int64_t g = 3 * (int64_t)cus;
+  return (int)(need < 1 ? 1 : (need < g ? need : g));
+}
+
 template <int XF>
 static void launch_fwd_xf(const LnParams& p, int out_dtype, hipStream_t s) {
-  const dim3 g(row_grid(p.R)), b(LN_THREADS);
+  const dim3 b(LN_THREADS);
+  if constexpr (XF != kF32) {
+    if (p.D > LN_PIPE_D / 2 && p.D <= LN_PIPE_D) {
+      const dim3 g(pipe_grid(p.R));
+      if (p.D == LN_PIPE_D) {
+        if (out_dtype == kE4M3) hipLaunchKernelGGL((ln_fwd_pipe_kernel<XF, kE4M3, true>), g, b, 0, s, p);
+        else if (out_dtype == kE5M2) hipLaunchKernelGGL((ln_fwd_pipe_kernel<XF, kE5M2, true>), g, b, 0, s, p);
+        else hipLaunchKernelGGL((ln_fwd_pipe_kernel<XF, kF16, true>), g, b, 0, s, p);
+      } else {
+        if (out_dtype == kE4M3) hipLaunchKernelGGL((ln_fwd_pipe_kernel<XF, kE4M3, false>), g, b, 0, s, p);
+        else if (out_dtype == kE5M2) hipLaunchKernelGGL((ln_fwd_pipe_kernel<XF, kE5M2, false>), g, b, 0, s, p);
+        else hipLaunchKernelGGL((ln_fwd_pipe_kernel<XF, kF16, false>), g, b, 0, s, p);
+      }
+      return;
+    }
+  }
+  const dim3 g(row_grid(p.R));
   if (out_dtype == kE4M3) hipLaunchKernelGGL((ln_fwd_kernel<XF, kE4M3>), g, b, 0, s, p);
   else if (out_dtype == kE5M2) hipLaunchKernelGGL((ln_fwd_kernel<XF, kE5M2>), g, b, 0, s, p);
   else hipLaunchKernelGGL((ln_fwd_kernel<XF, kF16>), g, b, 0, s, p);

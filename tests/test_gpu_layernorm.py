@@ -104,6 +104,11 @@ FWD_CASES = [
     (7, 4097, sc.E5M2, sc.E5M2, False, 0.5),
     (300, 4096, sc.F16, sc.E4M3, True, 1e-5),
     (1030, 256, sc.F32, sc.F16, True, 1e-3),
+    # rows of 2049 .. 4096 FP16 / FP8 elements: the pipelined kernel (several
+    # rows per wave, a ragged last chunk)
+    (5000, 2112, sc.F16, sc.E5M2, True, 1e-5),
+    (11, 3001, sc.E4M3, sc.F16, True, 0.0),
+    (2100, 2049, sc.E5M2, sc.E4M3, False, 1e-5),
 ]
 
 
