@@ -24,6 +24,8 @@
 #include "ew_util.h"
 #include "layernorm.h"
 
+#include <type_traits>
+
 namespace scalify {
 
 constexpr int LN_THREADS = 256;   // 4 waves: 4 rows at a time
@@ -349,6 +351,146 @@ __global__ __launch_bounds__(LN_THREADS) void ln_bwd_stats_kernel(LnParams p) {
     atomicMax(p.hdr, __float_as_uint(fmaxf(fmaxf(wmax[0], wmax[1]), fmaxf(wmax[2], wmax[3]))));
 }
 
+// The backward's statistics for rows of 2049 .. 4096 FP16 / FP8 elements,
+// each row of x and dy read from HBM once: the wave holds both rows' raw
+// codes in registers and loads the next rows of its stride while it computes
+// these (two buffers); gamma sits in LDS. Same arithmetic, in the same order,
+// as ln_bwd_stats_kernel.
+template <int XF, int DYF, bool FULL>
+__global__ __launch_bounds__(LN_THREADS) void ln_bwd_stats_pipe_kernel(LnParams p) {
+  constexpr int NJ = LN_PIPE_NJ;
+  constexpr int WX = XF == kF16 ? 8 : 4;    // dwords per 16-element chunk
+  constexpr int WD = DYF == kF16 ? 8 : 4;
+  __shared__ __attribute__((aligned(16))) float s_g[LN_PIPE_D];
+  __shared__ float wmax[4];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int D = p.D;
+  const int nch = (D + 15) / 16;
+  for (int e = threadIdx.x; e < 16 * nch; e += LN_THREADS) s_g[e] = (p.gamma && e < D) ? p.gamma[e] : 1.0f;
+  __syncthreads();
+  float4* rowstats = (float4*)p.partial;
+  const int64_t stride = (int64_t)gridDim.x * 4;
+  auto load_chunks = [&](auto fmt_tag, const void* base, int64_t ld, int64_t r, auto& w) {
+    constexpr int F = decltype(fmt_tag)::value;
+    constexpr int W = F == kF16 ? 8 : 4;
+    constexpr int EPW = F == kF16 ? 2 : 4;  // elements per dword
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int q = lane + 64 * j;
+      const int valid = D - 16 * q;
+#pragma unroll
+      for (int k = 0; k < W; ++k) w[j][k] = 0u;
+      if (r < p.R && (FULL || q < nch)) {
+        const int64_t e = r * ld + 16 * q;
+        if (FULL || valid >= 16) {
+#pragma unroll
+          for (int h = 0; h < W / 4; ++h) {
+            const u4 v = F == kF16 ? *((const u4*)((const uint16_t*)base + e) + h)
+                                   : *((const u4*)((const uint8_t*)base + e) + h);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) w[j][4 * h + k] = v[k];
+          }
+        } else {
+#pragma unroll
+          for (int i = 0; i < 16; ++i)
+            if (i < valid) w[j][i / EPW] |= load1<F>(base, e + i) << ((32 / EPW) * (i % EPW));
+        }
+      }
+    }
+  };
+  float lmax = 0.0f;
+  auto process = [&](int64_t r, const uint32_t (&wx)[NJ][WX], const uint32_t (&wd)[NJ][WD]) {
+    float s = 0.0f;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      if (FULL || lane + 64 * j < nch) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) s += ln_raw_decode<XF>(wx[j], i);
+      }
+    const float mu = wave_sum(s) / (float)D;
+    float t = 0.0f;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int q = lane + 64 * j;
+      if (FULL || q < nch) {
+        const int valid = FULL ? 16 : D - 16 * q;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const float d = ln_raw_decode<XF>(wx[j], i) - mu;
+          t += i < valid ? d * d : 0.0f;
+        }
+      }
+    }
+    const float sigma = sqrtf(wave_sum(t) / (float)D);
+    const float inv = 1.0f / (sigma + p.eps);
+    float sg = 0.0f, sgx = 0.0f;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int q = lane + 64 * j;
+      if (FULL || q < nch) {
+        const int n = 16 * q;
+        const int valid = FULL ? 16 : D - n;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const float g = i < valid ? ln_raw_decode<DYF>(wd[j], i) * s_g[n + i] : 0.0f;
+          sg += g;
+          sgx += g * ((ln_raw_decode<XF>(wx[j], i) - mu) * inv);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    sg = wave_sum(sg);
+    sgx = wave_sum(sgx);
+    float4 st;
+    st.x = mu;
+    st.y = inv;
+    st.z = sg / (float)D;
+    st.w = sigma > 0.0f ? (sgx / (float)D) / sigma : 0.0f;
+    if (lane == 0) rowstats[r] = st;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int q = lane + 64 * j;
+      if (FULL || q < nch) {
+        const int n = 16 * q;
+        const int valid = FULL ? 16 : D - n;
+        float dx[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          dx[i] = ln_dx(ln_raw_decode<XF>(wx[j], i), ln_raw_decode<DYF>(wd[j], i), s_g[n + i], st);
+          if (i < valid) lmax = fmaxf(lmax, fabsf(dx[i]));  // fmaxf skips NaN
+        }
+        if (p.pre_out) ln_store_f32(p.pre_out + r * (int64_t)D + n, valid, dx);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  using XT = std::integral_constant<int, XF>;
+  using DT = std::integral_constant<int, DYF>;
+  uint32_t xa[NJ][WX], xb[NJ][WX], da[NJ][WD], db[NJ][WD];
+  int64_t r = (int64_t)blockIdx.x * 4 + wave;
+  load_chunks(XT{}, p.x, p.ldx, r, xa);
+  load_chunks(DT{}, p.dy, p.lddy, r, da);
+#pragma unroll 1
+  while (r < p.R) {
+    load_chunks(XT{}, p.x, p.ldx, r + stride, xb);
+    load_chunks(DT{}, p.dy, p.lddy, r + stride, db);
+    process(r, xa, da);
+    r += stride;
+    if (r >= p.R) break;
+    load_chunks(XT{}, p.x, p.ldx, r + stride, xa);
+    load_chunks(DT{}, p.dy, p.lddy, r + stride, da);
+    process(r, xb, db);
+    r += stride;
+  }
+  // amax of |dx|: wave butterfly, the four waves, one atomic max per workgroup
+  for (int off = 32; off > 0; off >>= 1) lmax = fmaxf(lmax, __shfl_xor(lmax, off, 64));
+  if (lane == 0) wmax[wave] = lmax;
+  __syncthreads();
+  if (threadIdx.x == 0)
+    atomicMax(p.hdr, __float_as_uint(fmaxf(fmaxf(wmax[0], wmax[1]), fmaxf(wmax[2], wmax[3]))));
+}
+
 // Tile (row block blockIdx.y of LN_TILE_ROWS rows, column block blockIdx.x of
 // LN_TILE_COLS columns): dx recomputed from the row numbers, cast with the
 // rescale, and the tile's partial parameter gradients.
@@ -511,10 +653,28 @@ static void launch_apply_x(const LnParams& p, int out_dtype, dim3 g, dim3 b, hip
   else launch_apply<XF, kE5M2>(p, out_dtype, g, b, s);
 }
 
+template <int XF, int DYF>
+static void launch_stats_pipe(const LnParams& p, hipStream_t s) {
+  const dim3 g(pipe_grid(p.R)), b(LN_THREADS);
+  if (p.D == LN_PIPE_D) hipLaunchKernelGGL((ln_bwd_stats_pipe_kernel<XF, DYF, true>), g, b, 0, s, p);
+  else hipLaunchKernelGGL((ln_bwd_stats_pipe_kernel<XF, DYF, false>), g, b, 0, s, p);
+}
+
+template <int XF>
+static void launch_stats_pipe_x(const LnParams& p, hipStream_t s) {
+  if (p.dy_fmt == kF16) launch_stats_pipe<XF, kF16>(p, s);
+  else if (p.dy_fmt == kE4M3) launch_stats_pipe<XF, kE4M3>(p, s);
+  else launch_stats_pipe<XF, kE5M2>(p, s);
+}
+
 hipError_t launch_layernorm_bwd(const LnParams& p, const float* s_dy, const float* s_x,
                                 int out_dtype, hipStream_t s) {
   hipLaunchKernelGGL(ln_bwd_prologue_kernel, dim3(1), dim3(64), 0, s, p.hdr, s_dy, s_x);
-  if (p.R > 0) {
+  if (p.R > 0 && p.x_fmt != kF32 && p.dy_fmt != kF32 && p.D > LN_PIPE_D / 2 && p.D <= LN_PIPE_D) {
+    if (p.x_fmt == kF16) launch_stats_pipe_x<kF16>(p, s);
+    else if (p.x_fmt == kE4M3) launch_stats_pipe_x<kE4M3>(p, s);
+    else launch_stats_pipe_x<kE5M2>(p, s);
+  } else if (p.R > 0) {
     const dim3 g(row_grid(p.R)), b(LN_THREADS);
     if (p.x_fmt == kF16) hipLaunchKernelGGL((ln_bwd_stats_kernel<kF16>), g, b, 0, s, p);
     else if (p.x_fmt == kF32) hipLaunchKernelGGL((ln_bwd_stats_kernel<kF32>), g, b, 0, s, p);

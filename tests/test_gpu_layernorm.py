@@ -215,6 +215,12 @@ BWD_CASES = [
     (5, 8192, sc.E5M2, sc.F16, sc.E5M2, True, 1e-5, sc.RESCALE_AMAX),
     (7, 4097, sc.E4M3, sc.E5M2, sc.E4M3, False, 0.5, sc.RESCALE_AMAX),
     (1030, 256, sc.F16, sc.F32, sc.F16, True, 1e-3, sc.RESCALE_AMAX),
+    # rows of 2049 .. 4096 FP16 / FP8 elements: the pipelined statistics
+    # kernel (several rows per wave, ragged last chunks, D = 4096 whole)
+    (3000, 4096, sc.E5M2, sc.F16, sc.E5M2, True, 1e-5, sc.RESCALE_AMAX),
+    (2500, 2112, sc.F16, sc.E4M3, sc.E4M3, True, 1e-5, sc.RESCALE_AMAX),
+    (9, 3001, sc.E4M3, sc.E5M2, sc.F16, False, 0.0, sc.RESCALE_NONE),
+    (17, 2049, sc.F16, sc.F16, sc.E5M2, True, 1e-5, sc.RESCALE_AMAX),
 ]
 
 
