@@ -173,6 +173,17 @@ __global__ __launch_bounds__(LN_THREADS) void ln_fwd_kernel(LnParams p) {
 constexpr int LN_PIPE_NJ = 4;
 constexpr int LN_PIPE_D = 1024 * LN_PIPE_NJ;
 
+// An empty asm on the raw codes before each pass over them: the compiler then
+// decodes them again instead of keeping every decoded value of the row
+// alive across the passes (which would cost the occupancy).
+template <int NJ, int W>
+__device__ __forceinline__ void ln_opaque(uint32_t (&w)[NJ][W]) {
+#pragma unroll
+  for (int j = 0; j < NJ; ++j)
+#pragma unroll
+    for (int k = 0; k < W; ++k) asm volatile("" : "+v"(w[j][k]));
+}
+
 template <int XF>
 __device__ __forceinline__ float ln_raw_decode(const uint32_t* w, int i) {
   if constexpr (XF == kF16) return decode_hw<kF16>((w[i >> 1] >> (16 * (i & 1))) & 0xFFFFu);
@@ -224,7 +235,7 @@ __global__ __launch_bounds__(LN_THREADS) void ln_fwd_pipe_kernel(LnParams p) {
       }
     }
   };
-  auto process = [&](int64_t r, const uint32_t (&w)[NJ][WPC]) {
+  auto process = [&](int64_t r, uint32_t (&w)[NJ][WPC]) {
     float s = 0.0f;
 #pragma unroll
     for (int j = 0; j < NJ; ++j)
@@ -356,8 +367,10 @@ __global__ __launch_bounds__(LN_THREADS) void ln_bwd_stats_kernel(LnParams p) {
 // codes in registers and loads the next rows of its stride while it computes
 // these (two buffers); gamma sits in LDS. Same arithmetic, in the same order,
 // as ln_bwd_stats_kernel.
+// (three waves per SIMD: at most 170 VGPRs)
 template <int XF, int DYF, bool FULL>
-__global__ __launch_bounds__(LN_THREADS) void ln_bwd_stats_pipe_kernel(LnParams p) {
+__global__ __launch_bounds__(LN_THREADS) __attribute__((amdgpu_waves_per_eu(3)))
+void ln_bwd_stats_pipe_kernel(LnParams p) {
   constexpr int NJ = LN_PIPE_NJ;
   constexpr int WX = XF == kF16 ? 8 : 4;    // dwords per 16-element chunk
   constexpr int WD = DYF == kF16 ? 8 : 4;
@@ -400,7 +413,7 @@ __global__ __launch_bounds__(LN_THREADS) void ln_bwd_stats_pipe_kernel(LnParams 
     }
   };
   float lmax = 0.0f;
-  auto process = [&](int64_t r, const uint32_t (&wx)[NJ][WX], const uint32_t (&wd)[NJ][WD]) {
+  auto process = [&](int64_t r, uint32_t (&wx)[NJ][WX], uint32_t (&wd)[NJ][WD]) {
     float s = 0.0f;
 #pragma unroll
     for (int j = 0; j < NJ; ++j)
@@ -409,6 +422,7 @@ __global__ __launch_bounds__(LN_THREADS) void ln_bwd_stats_pipe_kernel(LnParams 
         for (int i = 0; i < 16; ++i) s += ln_raw_decode<XF>(wx[j], i);
       }
     const float mu = wave_sum(s) / (float)D;
+    ln_opaque(wx);
     float t = 0.0f;
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
@@ -424,6 +438,7 @@ __global__ __launch_bounds__(LN_THREADS) void ln_bwd_stats_pipe_kernel(LnParams 
     }
     const float sigma = sqrtf(wave_sum(t) / (float)D);
     const float inv = 1.0f / (sigma + p.eps);
+    ln_opaque(wx);
     float sg = 0.0f, sgx = 0.0f;
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
@@ -448,6 +463,8 @@ __global__ __launch_bounds__(LN_THREADS) void ln_bwd_stats_pipe_kernel(LnParams 
     st.z = sg / (float)D;
     st.w = sigma > 0.0f ? (sgx / (float)D) / sigma : 0.0f;
     if (lane == 0) rowstats[r] = st;
+    ln_opaque(wx);
+    ln_opaque(wd);
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
       const int q = lane + 64 * j;
@@ -590,9 +607,9 @@ int64_t layernorm_ws_floats(int64_t R, int64_t D) {
   return 4 * R + layernorm_row_tiles(R) * 2 * layernorm_param_stride(D);
 }
 
-// Workgroups of the pipelined forward: three per CU, each wave walking rows
-// with the grid's stride.
-static int pipe_grid(int64_t R) {
+// Workgroups of the pipelined kernels: per_cu per CU (as many as their
+// registers let run at once), each wave walking rows with the grid's stride.
+static int pipe_grid(int64_t R, int per_cu) {
   static int cus = 0;  // (a benign race: every thread computes the same value)
   if (cus <= 0) {
     int dev = 0, n = 0;
@@ -602,7 +619,7 @@ static int pipe_grid(int64_t R) {
     cus = n;
   }
   const int64_t need = (R + 3) / 4;
-  const int64_t g = 3 * (int64_t)cus;
+  const int64_t g = (int64_t)per_cu * cus;
   return (int)(need < 1 ? 1 : (need < g ? need : g));
 }
 
@@ -611,7 +628,7 @@ static void launch_fwd_xf(const LnParams& p, int out_dtype, hipStream_t s) {
   const dim3 b(LN_THREADS);
   if constexpr (XF != kF32) {
     if (p.D > LN_PIPE_D / 2 && p.D <= LN_PIPE_D) {
-      const dim3 g(pipe_grid(p.R));
+      const dim3 g(pipe_grid(p.R, 3));
       if (p.D == LN_PIPE_D) {
         if (out_dtype == kE4M3) hipLaunchKernelGGL((ln_fwd_pipe_kernel<XF, kE4M3, true>), g, b, 0, s, p);
         else if (out_dtype == kE5M2) hipLaunchKernelGGL((ln_fwd_pipe_kernel<XF, kE5M2, true>), g, b, 0, s, p);
@@ -655,7 +672,7 @@ static void launch_apply_x(const LnParams& p, int out_dtype, dim3 g, dim3 b, hip
 
 template <int XF, int DYF>
 static void launch_stats_pipe(const LnParams& p, hipStream_t s) {
-  const dim3 g(pipe_grid(p.R)), b(LN_THREADS);
+  const dim3 g(pipe_grid(p.R, 3)), b(LN_THREADS);
   if (p.D == LN_PIPE_D) hipLaunchKernelGGL((ln_bwd_stats_pipe_kernel<XF, DYF, true>), g, b, 0, s, p);
   else hipLaunchKernelGGL((ln_bwd_stats_pipe_kernel<XF, DYF, false>), g, b, 0, s, p);
 }
