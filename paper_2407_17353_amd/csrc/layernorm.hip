@@ -24,6 +24,7 @@
 #include "ew_util.h"
 #include "layernorm.h"
 
+#include <stdlib.h>
 #include <type_traits>
 
 namespace scalify {
@@ -110,6 +111,9 @@ __device__ __forceinline__ void ln_store_f32(float* q, int valid, const float (&
 template <int XF>
 __device__ __forceinline__ void ln_row_stats(const LnParams& p, int64_t r, int lane, float& mu,
                                              float& sigma) {
+  // (no FMA contraction: every product and sum rounded on its own, so the
+  // single-read and multi-pass kernels round alike)
+#pragma clang fp contract(off)
   const int nch = (p.D + 15) / 16;
   float s = 0.0f;
 #pragma unroll 2
@@ -137,6 +141,9 @@ __device__ __forceinline__ void ln_row_stats(const LnParams& p, int64_t r, int l
 
 template <int XF, int OUTF>
 __global__ __launch_bounds__(LN_THREADS) void ln_fwd_kernel(LnParams p) {
+  // (no FMA contraction: every product and sum rounded on its own, so the
+  // single-read and multi-pass kernels round alike)
+#pragma clang fp contract(off)
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const bool sat = p.sat != 0;
@@ -192,6 +199,9 @@ __device__ __forceinline__ float ln_raw_decode(const uint32_t* w, int i) {
 
 template <int XF, int OUTF, bool FULL>
 __global__ __launch_bounds__(LN_THREADS) void ln_fwd_pipe_kernel(LnParams p) {
+  // (no FMA contraction: every product and sum rounded on its own, so the
+  // single-read and multi-pass kernels round alike)
+#pragma clang fp contract(off)
   constexpr int NJ = LN_PIPE_NJ;
   constexpr int WPC = XF == kF16 ? 8 : 4;  // dwords per 16-element chunk
   __shared__ __attribute__((aligned(16))) float s_g[LN_PIPE_D];
@@ -303,6 +313,9 @@ __device__ __forceinline__ float ln_dx(float x, float dy, float gam, const float
 
 template <int XF>
 __global__ __launch_bounds__(LN_THREADS) void ln_bwd_stats_kernel(LnParams p) {
+  // (no FMA contraction: every product and sum rounded on its own, so the
+  // single-read and multi-pass kernels round alike)
+#pragma clang fp contract(off)
   __shared__ float wmax[4];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -371,6 +384,9 @@ __global__ __launch_bounds__(LN_THREADS) void ln_bwd_stats_kernel(LnParams p) {
 template <int XF, int DYF, bool FULL>
 __global__ __launch_bounds__(LN_THREADS) __attribute__((amdgpu_waves_per_eu(3)))
 void ln_bwd_stats_pipe_kernel(LnParams p) {
+  // (no FMA contraction: every product and sum rounded on its own, so the
+  // single-read and multi-pass kernels round alike)
+#pragma clang fp contract(off)
   constexpr int NJ = LN_PIPE_NJ;
   constexpr int WX = XF == kF16 ? 8 : 4;    // dwords per 16-element chunk
   constexpr int WD = DYF == kF16 ? 8 : 4;
@@ -623,11 +639,18 @@ static int pipe_grid(int64_t R, int per_cu) {
   return (int)(need < 1 ? 1 : (need < g ? need : g));
 }
 
+// The single-read kernels unless SCALIFY_LN_SINGLE_READ=0 (read at each
+// call), which keeps the multi-pass ones for every width.
+static bool single_read_enabled() {
+  const char* v = getenv("SCALIFY_LN_SINGLE_READ");
+  return !(v && v[0] == '0' && v[1] == 0);
+}
+
 template <int XF>
 static void launch_fwd_xf(const LnParams& p, int out_dtype, hipStream_t s) {
   const dim3 b(LN_THREADS);
   if constexpr (XF != kF32) {
-    if (p.D > LN_PIPE_D / 2 && p.D <= LN_PIPE_D) {
+    if (p.D > LN_PIPE_D / 2 && p.D <= LN_PIPE_D && single_read_enabled()) {
       const dim3 g(pipe_grid(p.R, 3));
       if (p.D == LN_PIPE_D) {
         if (out_dtype == kE4M3) hipLaunchKernelGGL((ln_fwd_pipe_kernel<XF, kE4M3, true>), g, b, 0, s, p);
@@ -687,7 +710,8 @@ static void launch_stats_pipe_x(const LnParams& p, hipStream_t s) {
 hipError_t launch_layernorm_bwd(const LnParams& p, const float* s_dy, const float* s_x,
                                 int out_dtype, hipStream_t s) {
   hipLaunchKernelGGL(ln_bwd_prologue_kernel, dim3(1), dim3(64), 0, s, p.hdr, s_dy, s_x);
-  if (p.R > 0 && p.x_fmt != kF32 && p.dy_fmt != kF32 && p.D > LN_PIPE_D / 2 && p.D <= LN_PIPE_D) {
+  if (p.R > 0 && p.x_fmt != kF32 && p.dy_fmt != kF32 && p.D > LN_PIPE_D / 2 && p.D <= LN_PIPE_D &&
+      single_read_enabled()) {
     if (p.x_fmt == kF16) launch_stats_pipe_x<kF16>(p, s);
     else if (p.x_fmt == kE4M3) launch_stats_pipe_x<kE4M3>(p, s);
     else launch_stats_pipe_x<kE5M2>(p, s);

@@ -12,7 +12,9 @@ before the rescale in the backward). Checks:
   L3  dgamma and dbeta against the oracle within 2e-5 of the sums of the
       magnitudes of their terms.
 """
+import contextlib
 import math
+import os
 
 import numpy as np
 import pytest
@@ -295,3 +297,45 @@ def test_layernorm_transformer_layer_full_size():
     run = run_bwd(dyc, sc.E5M2, 0, xc, sc.F16, 0, sc.E5M2, gamma, 1e-5)
     w = check_bwd(run, dyc, sc.E5M2, 0, xc, sc.F16, 0, sc.E5M2, gamma, 1e-5, sc.RESCALE_AMAX)
     say(f"  bwd ok, worst err/tol {w:.3g}")
+
+
+@contextlib.contextmanager
+def _env(**kw):
+    old = {k: os.environ.get(k) for k in kw}
+    os.environ.update({k: str(v) for k, v in kw.items()})
+    try:
+        yield
+    finally:
+        for k, v in old.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+
+
+@pytest.mark.parametrize("R,D,xfmt,dyfmt,ofmt", [(640, 4096, sc.F16, sc.E5M2, sc.E4M3),
+                                                 (257, 3001, sc.E4M3, sc.F16, sc.E5M2),
+                                                 (96, 2049, sc.E5M2, sc.E4M3, sc.F16)],
+                         ids=lambda v: str(v))
+def test_single_read_kernels_equal_the_multi_pass_ones(R, D, xfmt, dyfmt, ofmt):
+    """The forward and the backward statistics that read each row once
+    (rows of 2049..4096 FP16 / FP8 elements) give the same bits as the
+    multi-pass kernels (SCALIFY_LN_SINGLE_READ=0): same arithmetic, same
+    order."""
+    say(f"case layernorm single-read vs multi-pass R={R} D={D}")
+    rng = np.random.default_rng(R + D)
+    xc = _codes(_values(R, D, 300 + D, loc=0.3, scale=2.0, spread=5), xfmt)
+    dyc = _codes(_values(R, D, 400 + D, scale=0.5, spread=4), dyfmt)
+    gamma = (rng.standard_normal(D) * 0.5 + 1.0).astype(np.float32)
+    beta = (rng.standard_normal(D) * 0.2).astype(np.float32)
+    f1 = run_fwd(xc, xfmt, ofmt, gamma, beta, 1e-5)
+    b1 = run_bwd(dyc, dyfmt, -2, xc, xfmt, 3, ofmt, gamma, 1e-5)
+    with _env(SCALIFY_LN_SINGLE_READ=0):
+        f0 = run_fwd(xc, xfmt, ofmt, gamma, beta, 1e-5)
+        b0 = run_bwd(dyc, dyfmt, -2, xc, xfmt, 3, ofmt, gamma, 1e-5)
+    assert np.array_equal(f1[0], f0[0]) and f1[1] == f0[1]
+    assert np.array_equal(f1[2].view(np.uint32), f0[2].view(np.uint32))
+    assert np.array_equal(b1[0], b0[0]) and b1[1] == b0[1] and b1[2] == b0[2]
+    for k in (3, 4, 5):
+        assert np.array_equal(b1[k].view(np.uint32), b0[k].view(np.uint32))
+    check_fwd(f1, xc, xfmt, ofmt, gamma, beta, 1e-5)
