@@ -29,6 +29,15 @@
 
 namespace scalify {
 
+// f(std::integral_constant<int, I>), ..., up to N - 1 (compile-time indices).
+template <int I, int N, typename F>
+__device__ __forceinline__ void ln_static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    ln_static_for<I + 1, N>(f);
+  }
+}
+
 constexpr int LN_THREADS = 256;   // 4 waves: 4 rows at a time
 constexpr int LN_TILE_ROWS = 32;  // apply kernel: rows per workgroup
 constexpr int LN_TILE_THREADS = 128;
@@ -193,8 +202,37 @@ __device__ __forceinline__ void ln_opaque(uint32_t (&w)[NJ][W]) {
 
 template <int XF>
 __device__ __forceinline__ float ln_raw_decode(const uint32_t* w, int i) {
-  if constexpr (XF == kF16) return decode_hw<kF16>((w[i >> 1] >> (16 * (i & 1))) & 0xFFFFu);
+  if constexpr (XF == kF32) return __uint_as_float(w[i]);
+  else if constexpr (XF == kF16) return decode_hw<kF16>((w[i >> 1] >> (16 * (i & 1))) & 0xFFFFu);
   else return decode_hw<XF>((w[i >> 2] >> (8 * (i & 3))) & 0xFFu);
+}
+
+// Dwords of a 16-element chunk of format F, and the chunk's raw codes at
+// element e of base (valid elements, the rest zero: codes that decode to 0).
+template <int F>
+constexpr int ln_chunk_words() { return F == kF32 ? 16 : (F == kF16 ? 8 : 4); }
+
+template <int F>
+__device__ __forceinline__ void ln_load_raw(const void* base, int64_t e, int valid,
+                                            uint32_t (&w)[ln_chunk_words<F>()]) {
+  constexpr int W = ln_chunk_words<F>();
+  constexpr int EPW = 16 / W;  // elements per dword
+#pragma unroll
+  for (int k = 0; k < W; ++k) w[k] = 0u;
+  if (valid >= 16) {
+#pragma unroll
+    for (int h = 0; h < W / 4; ++h) {
+      const u4 v = F == kF32 ? *((const u4*)((const uint32_t*)base + e) + h)
+                             : (F == kF16 ? *((const u4*)((const uint16_t*)base + e) + h)
+                                          : *((const u4*)((const uint8_t*)base + e) + h));
+#pragma unroll
+      for (int k = 0; k < 4; ++k) w[4 * h + k] = v[k];
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      if (i < valid) w[i / EPW] |= load1<F>(base, e + i) << ((32 / EPW) * (i % EPW));
+  }
 }
 
 template <int XF, int OUTF, bool FULL>
@@ -553,19 +591,40 @@ __global__ __launch_bounds__(LN_TILE_THREADS) void ln_bwd_apply_kernel(LnParams 
   for (int i = 0; i < 16; ++i) pg[i] = pb[i] = 0.0f;
   const int64_t r0 = (int64_t)blockIdx.y * LN_TILE_ROWS;
   const int64_t r1 = r0 + LN_TILE_ROWS < p.R ? r0 + LN_TILE_ROWS : p.R;
-#pragma unroll 1
-  for (int64_t r = r0; r < r1; ++r) {
-    const float4 st = rowstats[r];
-    float x[16], d[16], dx[16];
-    ln_chunk_f<XF>(p.x, r * p.ldx + n, valid, x);
-    ln_chunk_f<DYF>(p.dy, r * p.lddy + n, valid, d);
+  // The rows' raw codes go through a ring of PF slots: slot k holds row
+  // rb + k while it is computed and then receives row rb + k + PF, so PF
+  // rows' loads are in flight while one is computed (the per-row sums keep
+  // their row order).
+  constexpr int PF = 4;
+  uint32_t rx[PF][ln_chunk_words<XF>()], rd[PF][ln_chunk_words<DYF>()];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      dx[i] = ln_dx(x[i], d[i], gam[i], st);
-      pg[i] += d[i] * ((x[i] - st.x) * st.y);
-      pb[i] += d[i];
+  for (int k = 0; k < PF; ++k)
+    if (r0 + k < r1) {
+      ln_load_raw<XF>(p.x, (r0 + k) * p.ldx + n, valid, rx[k]);
+      ln_load_raw<DYF>(p.dy, (r0 + k) * p.lddy + n, valid, rd[k]);
     }
-    ln_store16<OUTF>(p.out, r * p.ldo + n, valid, dx, shift, scale, fast, sat);
+#pragma unroll 1
+  for (int64_t rb = r0; rb < r1; rb += PF) {
+    ln_static_for<0, PF>([&](auto K) {
+      constexpr int k = decltype(K)::value;
+      const int64_t r = rb + k;
+      if (r < r1) {
+        const float4 st = rowstats[r];
+        float dx[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const float x = ln_raw_decode<XF>(rx[k], i), d = ln_raw_decode<DYF>(rd[k], i);
+          dx[i] = ln_dx(x, d, gam[i], st);
+          pg[i] += d * ((x - st.x) * st.y);
+          pb[i] += d;
+        }
+        ln_store16<OUTF>(p.out, r * p.ldo + n, valid, dx, shift, scale, fast, sat);
+        if (r + PF < r1) {
+          ln_load_raw<XF>(p.x, (r + PF) * p.ldx + n, valid, rx[k]);
+          ln_load_raw<DYF>(p.dy, (r + PF) * p.lddy + n, valid, rd[k]);
+        }
+      }
+    });
   }
   if (p.dgamma || p.dbeta) {
     ln_store_f32(part + n, valid, pg);
