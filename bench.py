@@ -351,8 +351,9 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
-              "(the sharding design is described in DESIGN.md)", file=sys.stderr)
+        print("bench.py runs on one GPU only: the library has no multi-GPU path "
+              "(it would shard by output tiles, with one all-reduce of the amax per call)",
+              file=sys.stderr)
         sys.exit(2)
     import torch
     from paper_2407_17353_amd import binding as sc
