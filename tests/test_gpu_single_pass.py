@@ -191,3 +191,55 @@ def test_none_mode_needs_no_intermediate(fout):
         codes = codes.view(np.uint16)
     e_out = int(math.frexp(float(out.scale.item()))[1] - 1)
     check_p1(codes, e_out, float(amax.item()), acc.cpu().numpy(), K, -1, 2, fout, sc.RESCALE_NONE)
+
+
+def _direct(A_st, B_st, fmt, fout, mode, sat, want_acc, amax_in):
+    a = sc.ScaledArray(stored_with_padding(A_st, DEV), fmt, sc.scale_tensor(1, DEV))
+    b = sc.ScaledArray(stored_with_padding(B_st, DEV), fmt, sc.scale_tensor(-2, DEV))
+    M, K = a.shape
+    _, N = b.shape
+    out = sc.empty_scaled(M, N, fout, DEV)
+    acc = torch.empty((M, N), dtype=torch.float32, device=DEV) if want_acc else None
+    amax = torch.empty(1, dtype=torch.float32, device=DEV)
+    kw = {"amax_in": torch.tensor([amax_in], dtype=torch.float32, device=DEV)} \
+        if mode == sc.RESCALE_DELAYED else {}
+    sc.scalify_matmul(a, b, out, rescale=mode, saturate=sat, acc_out=acc, amax_out=amax, **kw)
+    torch.cuda.synchronize()
+    codes = out.data.cpu().numpy()
+    if fout == sc.F16:
+        codes = codes.view(np.uint16)
+    return (codes.copy(), float(out.scale.item()), float(amax.item()),
+            acc.cpu().numpy() if want_acc else None)
+
+
+@pytest.mark.parametrize("mode", [sc.RESCALE_NONE, sc.RESCALE_DELAYED])
+@pytest.mark.parametrize("fout", [sc.E4M3, sc.E5M2, sc.F16])
+@pytest.mark.parametrize("sat", [True, False], ids=["sat", "nosat"])
+def test_direct_cast_interior_path_equals_the_checked_path(mode, fout, sat):
+    """The direct cast of a wave tile inside the matrix (shift inside the
+    conversion window, no exported accumulator: saturation chosen per tile,
+    NaN groups on their own branch, FP16 through a clamp) gives the codes,
+    scale and statistic of the per-element path that the same call takes
+    when it exports its accumulators, which P1 checks against the oracle.
+    Heavy-range E5M2 inputs overflow the output formats; NaN and Inf
+    accumulators sit in interior wave tiles."""
+    say(f"case direct interior mode={mode} fout={fout} sat={sat}")
+    M, N, K = 512, 384, 256
+    A = _codes((M, K), sc.E5M2, 131, heavy=True).numpy().copy()
+    B = _codes((K, N), sc.E5M2, 132, heavy=True).numpy().copy()
+    A[3, 7] = 0x7F     # NaN row
+    A[9, 11] = 0x7C    # +Inf row ...
+    B[11, 2] = 0       # ... with Inf * 0 = NaN at (9, 2)
+    A[140, 5] = 0xFF   # -NaN row
+    A[260, 9] = 0xFC   # -Inf row
+    At, Bt = torch.from_numpy(A), torch.from_numpy(B)
+    stat = 3.0e4  # the delayed statistic: a shift inside the window
+    fast = _direct(At, Bt, sc.E5M2, fout, mode, sat, False, stat)
+    ref = _direct(At, Bt, sc.E5M2, fout, mode, sat, True, stat)
+    assert np.array_equal(fast[0], ref[0]), \
+        f"{np.count_nonzero(fast[0] != ref[0])} codes differ"
+    assert fast[1] == ref[1] and np.float32(fast[2]) == np.float32(ref[2])
+    e_out = int(math.frexp(ref[1])[1] - 1)
+    if mode == sc.RESCALE_NONE:
+        check_p1(ref[0], e_out, ref[2], ref[3], K, 1, -2, fout, mode, saturate=sat)
+    assert np.isnan(ref[3][3]).all() and np.isnan(ref[3][9, 2]) and np.isnan(ref[3][140]).all()
