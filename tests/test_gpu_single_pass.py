@@ -243,3 +243,27 @@ def test_direct_cast_interior_path_equals_the_checked_path(mode, fout, sat):
     if mode == sc.RESCALE_NONE:
         check_p1(ref[0], e_out, ref[2], ref[3], K, 1, -2, fout, mode, saturate=sat)
     assert np.isnan(ref[3][3]).all() and np.isnan(ref[3][9, 2]) and np.isnan(ref[3][140]).all()
+
+
+@pytest.mark.parametrize("single_pass", [0, 1], ids=["pair", "single"])
+@pytest.mark.parametrize("fout", [sc.E4M3, sc.E5M2, sc.F16])
+@pytest.mark.parametrize("sat", [True, False], ids=["sat", "nosat"])
+def test_dynamic_rescale_interior_path_equals_the_checked_path(single_pass, fout, sat):
+    """The dynamic rescale without an exported accumulator (interior wave
+    tiles stored without per-element checks, or held by the single pass)
+    gives the codes, scale and statistic of the same call with the export,
+    which P1 checks against the oracle."""
+    say(f"case dynamic interior single_pass={single_pass} fout={fout} sat={sat}")
+    M, N, K = 512, 384, 256
+    A = _codes((M, K), sc.E5M2, 141, heavy=True).numpy().copy()
+    B = _codes((K, N), sc.E5M2, 142, heavy=True).numpy().copy()
+    A[3, 7] = 0x7F
+    A[140, 5] = 0xFF
+    At, Bt = torch.from_numpy(A), torch.from_numpy(B)
+    with env(SCALIFY_SINGLE_PASS=single_pass):
+        fast = gpu_matmul(At, sc.E5M2, False, 1, Bt, sc.E5M2, False, -2, fout, saturate=sat,
+                          want_acc=False)
+        ref = gpu_matmul(At, sc.E5M2, False, 1, Bt, sc.E5M2, False, -2, fout, saturate=sat)
+    assert np.array_equal(fast[0], ref[0]), f"{np.count_nonzero(fast[0] != ref[0])} codes differ"
+    assert fast[1] == ref[1] and np.float32(fast[2]) == np.float32(ref[2])
+    check_p1(ref[0], ref[1], ref[2], ref[3], K, 1, -2, fout, saturate=sat)
