@@ -271,3 +271,24 @@ def test_subnormal_accumulators_single_shift(fout):
     record("mx_subnormal_p2", fout=FMT[fout], max_err=float(err.max()),
            max_l1=float(l1.max()), exact=int(np.count_nonzero(err == 0)), n=int(err.size))
     say(f"  P2 max |acc - ref| {err.max():.3g} (l1 max {l1.max():.3g}), exact {np.count_nonzero(err == 0)}")
+
+
+@pytest.mark.parametrize("mode", list(MODES))
+@pytest.mark.parametrize("fout", [sc.E4M3, sc.E5M2, sc.F16])
+def test_interior_path_equals_the_checked_path(mode, fout):
+    """Block-scaled calls without an exported accumulator (interior wave
+    tiles cast or stored without per-element checks, the single pass where
+    it runs) give the codes, scale and statistic of the same call with the
+    export, which P1 checks."""
+    M, N, K = 512, 384, 512
+    say(f"case mx interior {mode} fout={fout}")
+    A = _codes((M, K), 0, 960)
+    B = _codes((K, N), 1, 961)
+    PA = wl.mx_block_scales(M, K, 962)
+    PB = wl.mx_block_scales(N, K, 963)
+    fast = _mx_run(A, 0, False, -1, B, 1, False, 2, fout, PA, PB, MODES[mode], amax_in=3.0,
+                   want_acc=False)
+    run = _mx_run(A, 0, False, -1, B, 1, False, 2, fout, PA, PB, MODES[mode], amax_in=3.0)
+    assert np.array_equal(fast[0], run[0]), f"{np.count_nonzero(fast[0] != run[0])} codes differ"
+    assert fast[1] == run[1] and np.float32(fast[2]) == np.float32(run[2])
+    _check(run, A, 0, False, -1, B, 1, False, 2, fout, PA, PB, MODES[mode], amax_in=3.0)
