@@ -120,8 +120,8 @@ __device__ __forceinline__ void ln_store_f32(float* q, int valid, const float (&
 template <int XF>
 __device__ __forceinline__ void ln_row_stats(const LnParams& p, int64_t r, int lane, float& mu,
                                              float& sigma) {
-  // (no FMA contraction: every product and sum rounded on its own, so the
-  // single-read and multi-pass kernels round alike)
+  // (no FMA contraction: the fused multiply-adds are written out, the same
+  // in the single-read and multi-pass kernels, so both round alike)
 #pragma clang fp contract(off)
   const int nch = (p.D + 15) / 16;
   float s = 0.0f;
@@ -142,7 +142,7 @@ __device__ __forceinline__ void ln_row_stats(const LnParams& p, int64_t r, int l
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const float d = v[i] - mu;
-      t += i < valid ? d * d : 0.0f;
+      t = fmaf(i < valid ? d : 0.0f, d, t);  // (one rounding per term)
     }
   }
   sigma = sqrtf(wave_sum(t) / (float)p.D);
@@ -150,8 +150,8 @@ __device__ __forceinline__ void ln_row_stats(const LnParams& p, int64_t r, int l
 
 template <int XF, int OUTF>
 __global__ __launch_bounds__(LN_THREADS) void ln_fwd_kernel(LnParams p) {
-  // (no FMA contraction: every product and sum rounded on its own, so the
-  // single-read and multi-pass kernels round alike)
+  // (no FMA contraction: the fused multiply-adds are written out, the same
+  // in the single-read and multi-pass kernels, so both round alike)
 #pragma clang fp contract(off)
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -172,7 +172,7 @@ __global__ __launch_bounds__(LN_THREADS) void ln_fwd_kernel(LnParams p) {
       ln_param16(p.gamma, n, valid, 1.0f, g);
       ln_param16(p.beta, n, valid, 0.0f, b);
 #pragma unroll
-      for (int i = 0; i < 16; ++i) y[i] = (v[i] - mu) * inv * g[i] + b[i];
+      for (int i = 0; i < 16; ++i) y[i] = fmaf((v[i] - mu) * inv, g[i], b[i]);
       if (p.pre_out) ln_store_f32(p.pre_out + r * (int64_t)p.D + n, valid, y);
       ln_store16<OUTF>(p.out, r * p.ldo + n, valid, y, 0, 1.0f, true, sat);
     }
@@ -237,8 +237,8 @@ __device__ __forceinline__ void ln_load_raw(const void* base, int64_t e, int val
 
 template <int XF, int OUTF, bool FULL>
 __global__ __launch_bounds__(LN_THREADS) void ln_fwd_pipe_kernel(LnParams p) {
-  // (no FMA contraction: every product and sum rounded on its own, so the
-  // single-read and multi-pass kernels round alike)
+  // (no FMA contraction: the fused multiply-adds are written out, the same
+  // in the single-read and multi-pass kernels, so both round alike)
 #pragma clang fp contract(off)
   constexpr int NJ = LN_PIPE_NJ;
   constexpr int WPC = XF == kF16 ? 8 : 4;  // dwords per 16-element chunk
@@ -301,7 +301,7 @@ __global__ __launch_bounds__(LN_THREADS) void ln_fwd_pipe_kernel(LnParams p) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const float d = ln_raw_decode<XF>(w[j], i) - mu;
-          t += i < valid ? d * d : 0.0f;
+          t = fmaf(i < valid ? d : 0.0f, d, t);  // (one rounding per term)
         }
       }
     }
@@ -316,7 +316,7 @@ __global__ __launch_bounds__(LN_THREADS) void ln_fwd_pipe_kernel(LnParams p) {
         float y[16];
 #pragma unroll
         for (int i = 0; i < 16; ++i)
-          y[i] = (ln_raw_decode<XF>(w[j], i) - mu) * inv * s_g[n + i] + s_b[n + i];
+          y[i] = fmaf((ln_raw_decode<XF>(w[j], i) - mu) * inv, s_g[n + i], s_b[n + i]);
         if (p.pre_out) ln_store_f32(p.pre_out + r * (int64_t)D + n, valid, y);
         ln_store16<OUTF>(p.out, r * p.ldo + n, valid, y, 0, 1.0f, true, sat);
       }
@@ -351,8 +351,8 @@ __device__ __forceinline__ float ln_dx(float x, float dy, float gam, const float
 
 template <int XF>
 __global__ __launch_bounds__(LN_THREADS) void ln_bwd_stats_kernel(LnParams p) {
-  // (no FMA contraction: every product and sum rounded on its own, so the
-  // single-read and multi-pass kernels round alike)
+  // (no FMA contraction: the fused multiply-adds are written out, the same
+  // in the single-read and multi-pass kernels, so both round alike)
 #pragma clang fp contract(off)
   __shared__ float wmax[4];
   const int lane = threadIdx.x & 63;
@@ -378,7 +378,7 @@ __global__ __launch_bounds__(LN_THREADS) void ln_bwd_stats_kernel(LnParams p) {
       for (int i = 0; i < 16; ++i) {
         const float g = i < valid ? d[i] * gam[i] : 0.0f;
         sg += g;
-        sgx += g * ((v[i] - mu) * inv);
+        sgx = fmaf(g, (v[i] - mu) * inv, sgx);
       }
     }
     sg = wave_sum(sg);
@@ -422,8 +422,8 @@ __global__ __launch_bounds__(LN_THREADS) void ln_bwd_stats_kernel(LnParams p) {
 template <int XF, int DYF, bool FULL>
 __global__ __launch_bounds__(LN_THREADS) __attribute__((amdgpu_waves_per_eu(3)))
 void ln_bwd_stats_pipe_kernel(LnParams p) {
-  // (no FMA contraction: every product and sum rounded on its own, so the
-  // single-read and multi-pass kernels round alike)
+  // (no FMA contraction: the fused multiply-adds are written out, the same
+  // in the single-read and multi-pass kernels, so both round alike)
 #pragma clang fp contract(off)
   constexpr int NJ = LN_PIPE_NJ;
   constexpr int WX = XF == kF16 ? 8 : 4;    // dwords per 16-element chunk
@@ -486,7 +486,7 @@ void ln_bwd_stats_pipe_kernel(LnParams p) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const float d = ln_raw_decode<XF>(wx[j], i) - mu;
-          t += i < valid ? d * d : 0.0f;
+          t = fmaf(i < valid ? d : 0.0f, d, t);  // (one rounding per term)
         }
       }
     }
@@ -504,7 +504,7 @@ void ln_bwd_stats_pipe_kernel(LnParams p) {
         for (int i = 0; i < 16; ++i) {
           const float g = i < valid ? ln_raw_decode<DYF>(wd[j], i) * s_g[n + i] : 0.0f;
           sg += g;
-          sgx += g * ((ln_raw_decode<XF>(wx[j], i) - mu) * inv);
+          sgx = fmaf(g, (ln_raw_decode<XF>(wx[j], i) - mu) * inv, sgx);
         }
       }
       __builtin_amdgcn_sched_barrier(0);
