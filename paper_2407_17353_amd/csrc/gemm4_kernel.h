@@ -33,6 +33,9 @@
 
 namespace scalify {
 
+// LDS bytes per wave for staging the epilogue's stores.
+constexpr int kStageWave = 4096;
+
 // Header words of the single-pass barrier (zeroed by the matmul prologue).
 constexpr int kHdrArrive = 5, kHdrState = 6, kHdrWritten = 7;
 enum SpState : uint32_t { SP_RUNNING = 0, SP_COMPLETE = 1, SP_ABORTED = 2 };
@@ -156,6 +159,7 @@ __global__ __launch_bounds__(256, 1) void gemm4_kernel(GemmParams p) {
   __shared__ __attribute__((aligned(1024))) uint8_t sB0[TILE_BYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t sA1[TILE_BYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t sB1[TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sStage[4 * kStageWave];
   __shared__ float red[4];
   __shared__ uint32_t sp_word[2];
 
@@ -377,6 +381,55 @@ __global__ __launch_bounds__(256, 1) void gemm4_kernel(GemmParams p) {
   // Block-scaled accumulators may be fp32 subnormals (the plain ones never are).
   auto fast_of = [&](int sh) { return sh >= (MX ? kFastShiftMinSub : -kFastShiftMax) && sh <= kFastShiftMax; };
 
+  // Stores of a wave tile inside the matrix, staged through the wave's own
+  // 4 KiB of LDS so that each store writes 16 bytes per lane and whole rows
+  // of the wave tile (a 16-row block of ESZ = 2 byte elements, or a 32-row
+  // block of 1 byte codes, per round). group(t) gives the packed elements
+  // of accumulator tile t (4 of them: 4 ESZ bytes) and folds the statistic;
+  // a lane writes them at its row and column, the 16-byte chunks of a row
+  // permuted by the row (XOR) so that the writes and the row reads spread
+  // over the LDS banks. LDS instructions of one wave complete in order, so
+  // a round's writes reuse the region after the previous round's reads.
+  auto staged = [&](auto esz_tag, uint8_t* base, int64_t ld, int m0, int n0, auto&& group) {
+    constexpr int ESZ = decltype(esz_tag)::value;
+    constexpr int RB = 128 * ESZ;    // bytes of a wave-tile row
+    constexpr int CPR = RB / 16;     // 16-byte chunks per row
+    constexpr int MPR = 2 / ESZ;     // accumulator-tile rows (of 16) per round
+    constexpr int LPR = 64 / CPR;    // rows per read
+    uint8_t* st = sStage + wave * kStageWave;
+    const int r = lane & 15, q = lane >> 4;
+    static_for<0, MI / MPR>([&](auto RD) {
+      constexpr int rd = decltype(RD)::value;
+      static_for<0, MPR * NI>([&](auto I) {
+        constexpr int i = decltype(I)::value;
+        constexpr int mi = rd * MPR + i / NI, ni = i % NI;
+        const int rr = 16 * (mi % MPR) + r;
+        const int chunk = ESZ == 2 ? 2 * ni + (q >> 1) : ni;
+        const int off = ESZ == 2 ? 8 * (q & 1) : 4 * q;
+        uint8_t* a = st + rr * RB + 16 * (chunk ^ (rr & (CPR - 1))) + off;
+        const auto w = group(std::integral_constant<int, mi * NI + ni>{});
+        if constexpr (ESZ == 2)
+          *(v2i*)a = w;
+        else
+          *(uint32_t*)a = w;
+      });
+      wait_lgkmcnt<0>();
+      u4 d[4];
+      static_for<0, 4>([&](auto J) {
+        constexpr int j = decltype(J)::value;
+        const int R = j * LPR + lane / CPR, cc = lane % CPR;
+        d[j] = *(const u4*)(st + R * RB + 16 * (cc ^ (R & (CPR - 1))));
+      });
+      wait_lgkmcnt<0>();
+      static_for<0, 4>([&](auto J) {
+        constexpr int j = decltype(J)::value;
+        const int R = j * LPR + lane / CPR, cc = lane % CPR;
+        const int64_t row = m0 + wm + 16 * rd * MPR + R;
+        *(u4*)(base + (row * ld + n0 + wn + cc * (16 / ESZ)) * ESZ) = d[j];
+      });
+    });
+  };
+
   // Store the tile at (m0, n0) from the accumulators: OUTF < 0 the
   // intermediate of EPI, else output codes of format OUTF with `shift`;
   // fold |acc| of the valid elements into lmax; ZERO: clear the
@@ -428,6 +481,10 @@ __global__ __launch_bounds__(256, 1) void gemm4_kernel(GemmParams p) {
       }
     };
     const bool inside = !p.acc_out && m0 + wm + 16 * MI <= M && n0 + wn + 16 * NI <= N;
+    // the staged stores write 16 aligned bytes per lane
+    const bool stage_ok = OUTF < 0 ? (p.ldw & 7) == 0 && ((uintptr_t)p.inter & 15) == 0
+                                   : ((p.ldc * (OUTF == kF16 ? 2 : 1)) & 15) == 0 &&
+                                         ((uintptr_t)p.out & 15) == 0;
     if constexpr (OUTF >= 0) {
       // Codes of a wave tile inside the matrix with the shift inside the fast
       // window: the conversion scales by itself, saturation is chosen once
@@ -435,13 +492,12 @@ __global__ __launch_bounds__(256, 1) void gemm4_kernel(GemmParams p) {
       // puts the NaN codes in and keeps the NaN out of the statistic.
       auto codes = [&](auto sat_tag) {
         constexpr bool SAT = decltype(sat_tag)::value;
-        static_for<0, MI * NI>([&](auto I) {
+        constexpr int ESZ = OUTF == kF16 ? 2 : 1;
+        staged(std::integral_constant<int, ESZ>{}, (uint8_t*)p.out, p.ldc, m0, n0, [&](auto I) {
           constexpr int t = decltype(I)::value;
-          constexpr int mi = t / NI, ni = t % NI;
           const v4f v = AccTile<t>::read();
           if constexpr (ZERO) AccTile<t>::zero();
           float x[4] = {v[0], v[1], v[2], v[3]};
-          const int64_t e = (int64_t)(mb + 16 * mi) * p.ldc + nb + 16 * ni;
           if constexpr (OUTF == kF16) {
             v2i w = cvt4_f16_fast<SAT>(x[0], x[1], x[2], x[3], inv);
             if (__builtin_expect(x[0] != x[0] || x[1] != x[1] || x[2] != x[2] || x[3] != x[3], 0)) {
@@ -455,7 +511,8 @@ __global__ __launch_bounds__(256, 1) void gemm4_kernel(GemmParams p) {
                 }
               w = v2i{(int)(h[0] | (h[1] << 16)), (int)(h[2] | (h[3] << 16))};
             }
-            *(v2i*)((uint16_t*)p.out + e) = w;
+            lmax = max3_abs(max3_abs(lmax, x[0], x[1]), x[2], x[3]);
+            return w;
           } else {
             uint32_t w = cast4_fp8_hw<OUTF>(__float_as_uint(x[0]), __float_as_uint(x[1]),
                                             __float_as_uint(x[2]), __float_as_uint(x[3]), scale, SAT);
@@ -468,16 +525,35 @@ __global__ __launch_bounds__(256, 1) void gemm4_kernel(GemmParams p) {
                   x[i] = 0.f;
                 }
             }
-            *(uint32_t*)((uint8_t*)p.out + e) = w;
+            lmax = max3_abs(max3_abs(lmax, x[0], x[1]), x[2], x[3]);
+            return w;
           }
-          lmax = max3_abs(max3_abs(lmax, x[0], x[1]), x[2], x[3]);
         });
       };
-      if (inside && fast) {
+      if (inside && fast && stage_ok) {
         if (sat)
           codes(std::true_type{});
         else
           codes(std::false_type{});
+        return;
+      }
+    }
+    if constexpr (OUTF < 0 && EPI == EPI_INTER16) {
+      if (inside && stage_ok) {
+        staged(std::integral_constant<int, 2>{}, (uint8_t*)p.inter, p.ldw, m0, n0, [&](auto I) {
+          constexpr int t = decltype(I)::value;
+          const v4f v = AccTile<t>::read();
+          if constexpr (ZERO) AccTile<t>::zero();
+          lmax = fmaxf(lmax, fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))));
+          uint32_t x[4];
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const uint32_t u = __float_as_uint(v[k]);
+            x[k] = u | ((u & 0xFFFFu) + 0xFFFFu);  // sticky16(u) in bits 16..
+          }
+          return v2i{(int)__builtin_amdgcn_perm(x[1], x[0], 0x07060302u),
+                     (int)__builtin_amdgcn_perm(x[3], x[2], 0x07060302u)};
+        });
         return;
       }
     }
@@ -639,8 +715,9 @@ __global__ __launch_bounds__(256, 1) void gemm4_kernel(GemmParams p) {
     // CH chunks per batch held as raw 16-byte words; right after a chunk is
     // cast and stored, the load of the same slot one batch ahead is issued,
     // so CH chunks per thread (64 KiB per CU) stay in flight. The first
-    // batch of the workgroup's own tiles is loaded before the barrier wait
-    // (its own stores, visible to the workgroup after the barrier above).
+    // batch of the workgroup's own tiles is loaded after the arrival, before
+    // the barrier wait (its own stores, visible to the workgroup after the
+    // barrier above).
     constexpr int U = EPI == EPI_INTER32 ? 4 : 2;   // 16-byte words per chunk
     constexpr int CH = EPI == EPI_INTER32 ? 4 : 8;   // chunks per batch (64 VGPRs)
     constexpr int BPT = 16 / CH;                     // batches per tile
@@ -660,9 +737,13 @@ __global__ __launch_bounds__(256, 1) void gemm4_kernel(GemmParams p) {
         for (int h = 0; h < U; ++h) raw[i][h] = q[h];
       }
     };
-    auto cast_slot = [&](auto I, int m0, int n0, int sub, int shift, bool fast, float scale,
-                         float inv) {
+    // MODE 0: any shift (encode16_any); 1 / 2: the shift inside the fast
+    // window, saturating / not (the conversion scales by itself; a group
+    // holding a NaN takes a branch that puts the NaN codes in)
+    auto cast_slot = [&](auto I, auto mode_tag, int m0, int n0, int sub, int shift, bool fast,
+                         float scale, float inv) {
       constexpr int i = decltype(I)::value;
+      constexpr int MODE = decltype(mode_tag)::value;
       const int m = m0 + (tid >> 4) + 16 * (sub * CH + i);
       const int n = n0 + 16 * (tid & 15);
       if (m < M && n < N) {
@@ -679,7 +760,44 @@ __global__ __launch_bounds__(256, 1) void gemm4_kernel(GemmParams p) {
             }
           }
         uint32_t w[8];
-        encode16_any<(OF < 0 ? kE4M3 : OF)>(c, fast, scale, inv, shift, sat, w);
+        if constexpr (MODE == 0) {
+          encode16_any<(OF < 0 ? kE4M3 : OF)>(c, fast, scale, inv, shift, sat, w);
+        } else {
+          constexpr bool SAT = MODE == 1;
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const uint32_t* u = c + 4 * g;
+            const bool nan = is_nan_bits(u[0]) || is_nan_bits(u[1]) || is_nan_bits(u[2]) ||
+                             is_nan_bits(u[3]);
+            if constexpr (OF == kF16) {
+              v2i h = cvt4_f16_fast<SAT>(__uint_as_float(u[0]), __uint_as_float(u[1]),
+                                         __uint_as_float(u[2]), __uint_as_float(u[3]), inv);
+              if (__builtin_expect(nan, 0)) {
+                uint32_t hh[4] = {(uint32_t)h.x & 0xFFFFu, (uint32_t)h.x >> 16,
+                                  (uint32_t)h.y & 0xFFFFu, (uint32_t)h.y >> 16};
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                  if (is_nan_bits(u[k])) hh[k] = FmtTraits<kF16>::NANC | ((u[k] >> 16) & 0x8000u);
+                h = v2i{(int)(hh[0] | (hh[1] << 16)), (int)(hh[2] | (hh[3] << 16))};
+              }
+              w[2 * g] = (uint32_t)h.x;
+              w[2 * g + 1] = (uint32_t)h.y;
+            } else {
+              constexpr int F = OF < 0 ? kE4M3 : OF;
+              uint32_t x = cast4_fp8_hw<F>(u[0], u[1], u[2], u[3], scale, SAT);
+              if (__builtin_expect(nan, 0)) {
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                  if (is_nan_bits(u[k])) {
+                    const uint32_t nc = FmtTraits<F>::NANC | ((u[k] >> 24) & 0x80u);
+                    x = (x & ~(0xFFu << (8 * k))) | (nc << (8 * k));
+                  }
+              }
+              w[g] = x;
+              w[4 + g] = 0u;
+            }
+          }
+        }
         const int64_t e = (int64_t)m * p.ldc + n;
         if (n + 16 <= N) {
           store_words16<SF>(p.out, e, w);
@@ -699,25 +817,27 @@ __global__ __launch_bounds__(256, 1) void gemm4_kernel(GemmParams p) {
       int cm0, cn0;  // origin of the batch being cast
       tile_of(all, 0, cm0, cn0);
       if (!loaded) static_for<0, CH>([&](auto I) { load_slot(I, cm0, cn0, 0); });
-      for (int bi = 0; bi < nb; ++bi) {
-        const int sub = bi % BPT, nbi = bi + 1, nsub = nbi % BPT;
-        int nm0 = cm0, nn0 = cn0;  // origin of the next batch
-        if (nbi < nb && nsub == 0) tile_of(all, nbi / BPT, nm0, nn0);
-        static_for<0, CH>([&](auto I) {
-          cast_slot(I, cm0, cn0, sub, shift, fast, scale, inv);
-          if (nbi < nb) load_slot(I, nm0, nn0, nsub);
-        });
-        cm0 = nm0;
-        cn0 = nn0;
-      }
+      auto batches = [&](auto mode_tag) {
+        for (int bi = 0; bi < nb; ++bi) {
+          const int sub = bi % BPT, nbi = bi + 1, nsub = nbi % BPT;
+          int nm0 = cm0, nn0 = cn0;  // origin of the next batch
+          if (nbi < nb && nsub == 0) tile_of(all, nbi / BPT, nm0, nn0);
+          static_for<0, CH>([&](auto I) {
+            cast_slot(I, mode_tag, cm0, cn0, sub, shift, fast, scale, inv);
+            if (nbi < nb) load_slot(I, nm0, nn0, nsub);
+          });
+          cm0 = nm0;
+          cn0 = nn0;
+        }
+      };
+      if (!fast)
+        batches(std::integral_constant<int, 0>{});
+      else if (sat)
+        batches(std::integral_constant<int, 1>{});
+      else
+        batches(std::integral_constant<int, 2>{});
     };
     const bool own = ntiles > 1;
-    if (own) {
-      int m0, n0;
-      tile_of(false, 0, m0, n0);
-      static_for<0, CH>([&](auto I) { load_slot(I, m0, n0, 0); });
-    }
-
     if (tid == 0) {
       const float wmax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
       __hip_atomic_fetch_max(p.hdr, __float_as_uint(wmax), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -733,6 +853,15 @@ __global__ __launch_bounds__(256, 1) void gemm4_kernel(GemmParams p) {
                                              __ATOMIC_RELAXED, __ATOMIC_RELAXED,
                                              __HIP_MEMORY_SCOPE_AGENT);
       }
+    }
+    // the first batch of the earlier tiles in flight during the wait (issued
+    // after the arrival, which waits for every load of its wave)
+    if (own) {
+      int m0, n0;
+      tile_of(false, 0, m0, n0);
+      static_for<0, CH>([&](auto I) { load_slot(I, m0, n0, 0); });
+    }
+    if (tid == 0) {
       uint32_t st = __hip_atomic_load(p.hdr + kHdrState, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       // (a poll takes at least the sleep, 640 cycles or 30 ticks: the poll
       // count bounds the wait even if the counter did not advance)
