@@ -207,6 +207,41 @@ __device__ __forceinline__ float ln_raw_decode(const uint32_t* w, int i) {
   else return decode_hw<XF>((w[i >> 2] >> (8 * (i & 3))) & 0xFFu);
 }
 
+// Element I of a chunk's raw codes as fp32: an FP8 code is converted straight
+// from its byte of the word (the conversion selects the byte).
+template <int XF, int I>
+__device__ __forceinline__ float ln_decode_at(const uint32_t* w) {
+  if constexpr (XF == kE4M3) return __builtin_amdgcn_cvt_scalef32_f32_fp8(w[I >> 2], 1.0f, I & 3);
+  else if constexpr (XF == kE5M2) return __builtin_amdgcn_cvt_scalef32_f32_bf8(w[I >> 2], 1.0f, I & 3);
+  else return ln_raw_decode<XF>(w, I);
+}
+
+// The 16 elements of a chunk's raw codes as fp32 (exact), FP8 codes two per
+// conversion (the packed form takes the low or the high 16 bits of a word).
+template <int XF>
+__device__ __forceinline__ void ln_decode16(const uint32_t* w, float (&x)[16]) {
+  if constexpr (XF == kE4M3 || XF == kE5M2) {
+    auto pk = [](uint32_t v, auto hi_tag) {
+      if constexpr (XF == kE4M3)
+        return __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(v, 1.0f, decltype(hi_tag)::value);
+      else
+        return __builtin_amdgcn_cvt_scalef32_pk_f32_bf8(v, 1.0f, decltype(hi_tag)::value);
+    };
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const auto lo = pk(w[k], std::false_type{});
+      const auto hi = pk(w[k], std::true_type{});
+      x[4 * k] = lo[0];
+      x[4 * k + 1] = lo[1];
+      x[4 * k + 2] = hi[0];
+      x[4 * k + 3] = hi[1];
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) x[i] = ln_raw_decode<XF>(w, i);
+  }
+}
+
 // Dwords of a 16-element chunk of format F, and the chunk's raw codes at
 // element e of base (valid elements, the rest zero: codes that decode to 0).
 template <int F>
@@ -500,12 +535,12 @@ void ln_bwd_stats_pipe_kernel(LnParams p) {
       if (FULL || q < nch) {
         const int n = 16 * q;
         const int valid = FULL ? 16 : D - n;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const float g = i < valid ? ln_raw_decode<DYF>(wd[j], i) * s_g[n + i] : 0.0f;
+        ln_static_for<0, 16>([&](auto I) {
+          constexpr int i = decltype(I)::value;
+          const float g = i < valid ? ln_decode_at<DYF, i>(wd[j]) * s_g[n + i] : 0.0f;
           sg += g;
-          sgx = fmaf(g, (ln_raw_decode<XF>(wx[j], i) - mu) * inv, sgx);
-        }
+          sgx = fmaf(g, (ln_decode_at<XF, i>(wx[j]) - mu) * inv, sgx);
+        });
       }
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -526,11 +561,11 @@ void ln_bwd_stats_pipe_kernel(LnParams p) {
         const int n = 16 * q;
         const int valid = FULL ? 16 : D - n;
         float dx[16];
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          dx[i] = ln_dx(ln_raw_decode<XF>(wx[j], i), ln_raw_decode<DYF>(wd[j], i), s_g[n + i], st);
+        ln_static_for<0, 16>([&](auto I) {
+          constexpr int i = decltype(I)::value;
+          dx[i] = ln_dx(ln_decode_at<XF, i>(wx[j]), ln_decode_at<DYF, i>(wd[j]), s_g[n + i], st);
           if (i < valid) lmax = fmaxf(lmax, fabsf(dx[i]));  // fmaxf skips NaN
-        }
+        });
         if (p.pre_out) ln_store_f32(p.pre_out + r * (int64_t)D + n, valid, dx);
       }
       __builtin_amdgcn_sched_barrier(0);
@@ -611,9 +646,12 @@ __global__ __launch_bounds__(LN_TILE_THREADS) void ln_bwd_apply_kernel(LnParams 
       if (r < r1) {
         const float4 st = rowstats[r];
         float dx[16];
+        float xv[16], dv[16];
+        ln_decode16<XF>(rx[k], xv);
+        ln_decode16<DYF>(rd[k], dv);
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          const float x = ln_raw_decode<XF>(rx[k], i), d = ln_raw_decode<DYF>(rd[k], i);
+          const float x = xv[i], d = dv[i];
           dx[i] = ln_dx(x, d, gam[i], st);
           pg[i] += d * ((x - st.x) * st.y);
           pb[i] += d;
