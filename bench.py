@@ -91,7 +91,7 @@ def copy_calibration(dev, nbytes=256 << 20, reps=5):
     del src, dst
 
 
-def settle_clock(call, stream, min_calls=80, max_calls=500, chunk=10, tol=0.01):
+def settle_clock(call, stream, min_calls=150, max_calls=500, chunk=10, tol=0.01):
     """Run `call` back to back until its duration is steady: at least
     min_calls calls, then until two consecutive `chunk`-call means agree
     within `tol` (at most max_calls). In a fresh process the chip's clock
@@ -99,7 +99,7 @@ def settle_clock(call, stream, min_calls=80, max_calls=500, chunk=10, tol=0.01):
     the 8192^3 GEMM run up to 37 % slower at the same cycle count) and then
     settles; this runs before the warm-up calls, untimed, and its record
     (calls made, the first calls' and the slowest and last chunk's mean
-    duration) goes into the bench line."""
+    duration, every chunk's mean) goes into the bench line."""
     import torch
     means, first, n = [], [], 0
     while n < max_calls:
@@ -117,7 +117,8 @@ def settle_clock(call, stream, min_calls=80, max_calls=500, chunk=10, tol=0.01):
             break
     return {"calls": n, "first_calls_us": [round(t * 1e3, 1) for t in first[:5]],
             "slowest_10_call_mean_us": round(max(means) * 1e3, 1),
-            "last_10_call_mean_us": round(means[-1] * 1e3, 1)}
+            "last_10_call_mean_us": round(means[-1] * 1e3, 1),
+            "10_call_means_us": [round(m * 1e3) for m in means]}
 
 
 def time_case(case, steps, warmup, dev, ws=None, mode=None, act=0, residual_seed=None,
