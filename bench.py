@@ -91,6 +91,12 @@ def copy_calibration(dev, nbytes=256 << 20, reps=5):
     del src, dst
 
 
+def settled(means, calls, min_calls=150, tol=0.01):
+    """The settling rule: at least min_calls calls made, and the last two
+    chunk means (ms) within tol of each other."""
+    return calls >= min_calls and len(means) >= 2 and abs(means[-1] - means[-2]) <= tol * means[-2]
+
+
 def settle_clock(call, stream, min_calls=150, max_calls=500, chunk=10, tol=0.01):
     """Run `call` back to back until its duration is steady: at least
     min_calls calls, then until two consecutive `chunk`-call means agree
@@ -113,7 +119,7 @@ def settle_clock(call, stream, min_calls=150, max_calls=500, chunk=10, tol=0.01)
         first = first or ts
         means.append(sum(ts) / chunk)
         n += chunk
-        if n >= min_calls and abs(means[-1] - means[-2]) <= tol * means[-2]:
+        if settled(means, n, min_calls, tol):
             break
     return {"calls": n, "first_calls_us": [round(t * 1e3, 1) for t in first[:5]],
             "slowest_10_call_mean_us": round(max(means) * 1e3, 1),
