@@ -671,18 +671,23 @@ __global__ __launch_bounds__(LN_TILE_THREADS) void ln_bwd_apply_kernel(LnParams 
 }
 
 // dgamma[j], dbeta[j] = fixed-order sums of the row tiles' partials: a
-// workgroup covers 64 columns; its 4 waves sum interleaved quarters of the
-// tiles (wave w: tiles w, w + 4, ...), then wave 0 adds the four in order.
-__global__ __launch_bounds__(256) void ln_params_kernel(const float* part, int tiles, int D,
-                                                        float* dgamma, float* dbeta) {
-  __shared__ float red[2][4][64];
+// workgroup covers 64 columns; its LN_PARAM_WAVES waves sum interleaved
+// shares of the tiles (wave w: tiles w, w + LN_PARAM_WAVES, ...), then wave
+// 0 adds the wave sums pairwise in a fixed tree. (Few columns, many tiles:
+// the waves of a workgroup keep more of the tiles' loads in flight.)
+constexpr int LN_PARAM_WAVES = 16;
+
+__global__ __launch_bounds__(64 * LN_PARAM_WAVES) void ln_params_kernel(const float* part, int tiles,
+                                                                        int D, float* dgamma,
+                                                                        float* dbeta) {
+  __shared__ float red[2][LN_PARAM_WAVES][64];
   const int c = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int j = blockIdx.x * 64 + c;
   const int64_t dp = layernorm_param_stride(D);
   float g = 0.0f, b = 0.0f;
   if (j < D) {
 #pragma unroll 8
-    for (int k = w; k < tiles; k += 4) {
+    for (int k = w; k < tiles; k += LN_PARAM_WAVES) {
       g += part[(int64_t)k * 2 * dp + j];
       b += part[(int64_t)k * 2 * dp + dp + j];
     }
@@ -691,10 +696,21 @@ __global__ __launch_bounds__(256) void ln_params_kernel(const float* part, int t
   red[1][w][c] = b;
   __syncthreads();
   if (w == 0 && j < D) {
-    const float sg = (red[0][0][c] + red[0][1][c]) + (red[0][2][c] + red[0][3][c]);
-    const float sb = (red[1][0][c] + red[1][1][c]) + (red[1][2][c] + red[1][3][c]);
-    if (dgamma) dgamma[j] = sg;
-    if (dbeta) dbeta[j] = sb;
+    float sg[LN_PARAM_WAVES], sb[LN_PARAM_WAVES];
+#pragma unroll
+    for (int i = 0; i < LN_PARAM_WAVES; ++i) {
+      sg[i] = red[0][i][c];
+      sb[i] = red[1][i][c];
+    }
+#pragma unroll
+    for (int h = 1; h < LN_PARAM_WAVES; h *= 2)
+#pragma unroll
+      for (int i = 0; i < LN_PARAM_WAVES; i += 2 * h) {
+        sg[i] += sg[i + h];
+        sb[i] += sb[i + h];
+      }
+    if (dgamma) dgamma[j] = sg[0];
+    if (dbeta) dbeta[j] = sb[0];
   }
 }
 
@@ -829,7 +845,8 @@ hipError_t launch_layernorm_bwd(const LnParams& p, const float* s_dy, const floa
   else if (p.x_fmt == kE4M3) launch_apply_x<kE4M3>(p, out_dtype, ga, ba, s);
   else launch_apply_x<kE5M2>(p, out_dtype, ga, ba, s);
   if ((p.dgamma || p.dbeta) && p.D > 0)
-    hipLaunchKernelGGL(ln_params_kernel, dim3((p.D + 63) / 64), dim3(256), 0, s, p.partial + 4 * p.R,
+    hipLaunchKernelGGL(ln_params_kernel, dim3((p.D + 63) / 64), dim3(64 * LN_PARAM_WAVES), 0, s,
+                       p.partial + 4 * p.R,
                        (int)tiles, p.D, p.dgamma, p.dbeta);
   return hipGetLastError();
 }
